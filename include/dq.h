@@ -1,0 +1,213 @@
+/*
+ * dq.h - C ABI of the MI355X (gfx950) hot path of disaggregated quantization:
+ * the phase-specific quantized linear layer (arXiv 2609.26333, Sec. 2.3
+ * "Format disaggregation"; App. A "Quantization formats"; App. C).
+ *
+ *   prefill:  dq_quantize_act_nvfp4 -> dq_prefill_gemm   (W4A4 NVFP4)
+ *   decode:   dq_decode_gemv                              (weight-only LUT, bf16 x)
+ *   offline:  dq_pack_nvfp4, dq_pack_lut3                 (weight packing)
+ *
+ * Conventions for every call
+ *   - Buffers are device memory owned by the caller.  The library allocates
+ *     nothing and keeps no state except a thread-local last-error string.
+ *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*;
+ *     NULL is the default stream).  Nothing synchronizes inside the library.
+ *   - Arguments are validated on the host before any HIP call; a rejected
+ *     call launches nothing and returns DQ_ERR_INVALID_ARG or
+ *     DQ_ERR_UNSUPPORTED.  A failed launch returns DQ_ERR_HIP.  Faults during
+ *     execution surface at the caller's next synchronization.
+ *   - Device pointers must be 16-byte aligned (scalar fp32 pointers: 4-byte).
+ *   - Inputs must be finite; results for non-finite inputs are unspecified
+ *     (no crash).
+ *   - Descriptor structs (dq_nvfp4_t, dq_lut_t) are host memory read during
+ *     the call only.
+ */
+#ifndef DQ_H
+#define DQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DQ_ABI_VERSION 1
+
+typedef int32_t dq_status;
+#define DQ_OK 0
+#define DQ_ERR_INVALID_ARG (-1) /* null/misaligned pointer, bad size or enum */
+#define DQ_ERR_UNSUPPORTED (-2) /* valid request this build does not implement */
+#define DQ_ERR_HIP (-3)         /* a HIP launch failed; see dq_last_error() */
+
+/* Output element kinds. */
+#define DQ_OUT_F32 0
+#define DQ_OUT_BF16 1
+#define DQ_OUT_NVFP4 2
+
+/* LUT modes. */
+#define DQ_LUT_PER_ROW 0    /* one 2^bits-entry fp16 table per output row */
+#define DQ_LUT_PAPER_GRID 1 /* fixed grid + signed E4M3 per 16 + fp32 global scale */
+
+/* GEMM epilogue flags. */
+#define DQ_EPI_SWIGLU 1
+
+/*
+ * NVFP4 tensor (App. A, "NVFP4-esque two-level scaling", "NVFP4").
+ * Logical content: rows x cols E2M1 codes (code = sign << 3 | index into
+ * {0, .5, 1, 1.5, 2, 3, 4, 6}; a zero magnitude has sign 0), one E4M3 scale
+ * per 16 consecutive columns of a row, one fp32 global scale G.  Element
+ * value = e2m1(code) * e4m3(scale) * G.  Columns are the contraction
+ * dimension K.
+ *
+ * Physical layout ("32x64 tiles").  Let R32 = rows rounded up to 32 and
+ * C64 = cols rounded up to 64.  Padding elements hold code 0 and scale 0.
+ *   codes:  R32*C64/2 bytes, tiles of 32 rows x 64 cols stored tile-row-major:
+ *           tile (tr, tc) starts at byte (tr*(C64/64) + tc) * 1024; inside it
+ *           row r (0..31) occupies bytes r*32 .. r*32+31 and byte j holds
+ *           column tc*64 + 2j in its low nibble and column tc*64 + 2j + 1 in
+ *           its high nibble.
+ *   scales: R32*C64/16 bytes, tile (tr, tc) starts at (tr*(C64/64) + tc) * 128;
+ *           row r, block b (0..3, columns tc*64 + 16b ..) is byte r*4 + b.
+ *   G:      one float.
+ */
+typedef struct dq_nvfp4 {
+  uint8_t* codes;
+  uint8_t* scales;
+  float* G;
+  int64_t rows;
+  int64_t cols;
+} dq_nvfp4_t;
+
+/*
+ * LUT weight (decode side; App. A "LUT formats" for PAPER_GRID; PER_ROW is
+ * the per-row equal-count table of the benchmark workloads).
+ * Logical content: rows x cols codes in [0, 2^bits).  Weight value:
+ *   PER_ROW:    lut[row * 2^bits + code]                       (fp16 table)
+ *   PAPER_GRID: grid[code] * e4m3(scale[row, col/16]) * G      (signed scale)
+ *
+ * Physical layout ("16x128 tiles").  Let R16 = rows rounded up to 16 and
+ * C128 = cols rounded up to 128; padding codes are 0 and padding table
+ * entries / scales are 0.
+ *   codes:  tile (tr, c) = rows 16tr..16tr+15, cols 128c..128c+127, stored at
+ *           byte (tr*(C128/128) + c) * 64 * G where G = 12 (bits 3) or 8
+ *           (bits 2) bytes per group.  Group g = q*16 + i (i = row in tile,
+ *           q = 0..3) holds the 32 codes of columns 128c + 32q + t, t = 0..31.
+ *           With s = t/4 and b = t%4, code t sits in little-endian dword w of
+ *           the group:
+ *             bits 3: s=0..5 -> dword s/2, bits [8b + 3(s%2), +3);
+ *                     s=6    -> dword 0 bits [8b+6, 8b+8) (low 2 bits) and
+ *                               dword 2 bit 8b+6 (high bit);
+ *                     s=7    -> dword 1 bits [8b+6, 8b+8) and dword 2 bit 8b+7.
+ *             bits 2: dword s/4, bits [8b + 2(s%4), +2).
+ *   lut:    PER_ROW: R16 * 2^bits fp16 (uint16 bit patterns), row-major.
+ *           PAPER_GRID: 2^bits fp16, ascending, containing one 0.
+ *   scales: PAPER_GRID only (NULL for PER_ROW): tile (tr, c) at byte
+ *           (tr*(C128/128) + c) * 128; group g = q*16 + i holds 2 bytes at
+ *           g*2: the signed E4M3 scales of column blocks 128c + 32q + 0..15
+ *           and + 16..31 of row 16tr + i.
+ *   G:      PAPER_GRID only: one float.
+ */
+typedef struct dq_lut {
+  uint8_t* codes;
+  uint16_t* lut;
+  uint8_t* scales;
+  float* G;
+  int64_t rows;
+  int64_t cols;
+  int32_t bits;
+  int32_t mode;
+} dq_lut_t;
+
+/* ---- diagnostics -------------------------------------------------------- */
+int dq_abi_version(void);
+const char* dq_status_string(dq_status s);
+/* Message of the last failing call on this thread ("" if none). */
+const char* dq_last_error(void);
+
+/* ---- size queries (host only) ------------------------------------------- */
+/* Bytes of the codes and scales buffers of a rows x cols NVFP4 tensor
+ * (cols % 16 == 0, rows >= 0). */
+dq_status dq_nvfp4_sizes(int64_t rows, int64_t cols, size_t* code_bytes, size_t* scale_bytes);
+/* Bytes of the codes, lut and scales buffers of a LUT weight
+ * (bits 2 or 3; cols % 32 == 0).  scale_bytes is 0 for PER_ROW. */
+dq_status dq_lut_sizes(int bits, int mode, int64_t rows, int64_t cols, size_t* code_bytes,
+                       size_t* lut_bytes, size_t* scale_bytes);
+
+/* ---- a2: weight packing, NVFP4 (App. A "NVFP4"; round to nearest) --------
+ * W: device fp32 [N, K] row-major (K contiguous), K % 16 == 0.
+ * G_override: device float or NULL.  NULL -> G = fp32(max|W| / 2688) is
+ *   computed on the device (1 if W is all zero).  Non-NULL -> that G is used,
+ *   e.g. the shared scale of a fused projection group.
+ * out: rows = N, cols = K, buffers sized by dq_nvfp4_sizes; out->G receives G.
+ * Per block of 16: t = fp32(max|w| / fp32(6G)); scale = E4M3(t) (nearest,
+ * ties to even, saturating at 448); S = fp32(e4m3 * G); codes =
+ * E2M1(fp32(w / S)) (nearest, ties to even, |y| >= 6 -> 6); S == 0 -> codes 0. */
+dq_status dq_pack_nvfp4(const float* W, int64_t N, int64_t K, const float* G_override,
+                        const dq_nvfp4_t* out, void* stream);
+
+/* ---- a5: weight packing, LUT (bits 3 = LUT3, bits 2 = LUT2) --------------
+ * W: device fp32 [N, K] row-major, K % 32 == 0.
+ * PER_ROW: each row is sorted, cut into 2^bits equal-count bins; entry j =
+ *   fp16(round-to-nearest-even of fp64(sum of bin j) / count); code =
+ *   #{j : w > (L_j + L_{j+1}) / 2} (nearest entry, ties to the lower index).
+ *   K <= 32768 (the row is sorted in LDS); larger K -> DQ_ERR_UNSUPPORTED.
+ * PAPER_GRID (App. A "LUT formats"): grid = host pointer to 2^bits fp16
+ *   values (ascending, one exactly 0) or NULL for the paper's grid rounded to
+ *   fp16; G = fp32(max|W| / 2688); per block of 16 the largest |w| (lowest k
+ *   on ties) sets d = sign(w*) * E4M3(fp32(|w*| / fp32(6G))), S = fp32(d G);
+ *   code = nearest grid level of fp32(w / S) (ties to the lower level);
+ *   S == 0 -> the zero level.
+ * out: rows = N, cols = K, bits, mode set by the caller; buffers sized by
+ *   dq_lut_sizes (PER_ROW: scales and G may be NULL). */
+dq_status dq_pack_lut3(const float* W, int64_t N, int64_t K, int bits, int mode,
+                       const uint16_t* grid, const dq_lut_t* out, void* stream);
+
+/* ---- a1: activation quantization to NVFP4 --------------------------------
+ * X: device bf16 [M, K] row-major (uint16 bit patterns), K % 16 == 0.
+ * G_static: device float or NULL.  Non-NULL: the static per-tensor input
+ *   scale of a running-maximum observer (App. A "NVFP4"); values beyond it
+ *   saturate.  NULL: dynamic, G = fp32(max|X| / 2688) from an extra pass.
+ * out: rows = M, cols = K; out->G receives the G used.  Same block rule as
+ * dq_pack_nvfp4. */
+dq_status dq_quantize_act_nvfp4(const uint16_t* X, int64_t M, int64_t K, const float* G_static,
+                                const dq_nvfp4_t* out, void* stream);
+
+/* ---- a3 (+a1 fused, +a4): W4A4 NVFP4 GEMM --------------------------------
+ * Y[m, n] = G_a * G_w * sum_k a[m, k] * w[n, k] over the dequantized NVFP4
+ * operands (exact products, fp32 accumulation).
+ * A: quantized activations (rows = M, cols = K) - or NULL together with
+ *   X (device bf16 [M, K]) and G_x_static (device float): the activations are
+ *   then quantized inside the GEMM with the static scale (fused a1).
+ *   Exactly one of A and X must be given.
+ * W: packed weights, rows = N, cols = K (same K as A).
+ * out_kind DQ_OUT_F32 / DQ_OUT_BF16: Y is device [M, N] row-major fp32 / bf16
+ *   (bf16: round to nearest even).
+ * out_kind DQ_OUT_NVFP4 (a4): the fp32 result is quantized along N in blocks
+ *   of 16 with the static scale *G_out_static into Yq (rows = M, cols = N, or
+ *   N/2 with DQ_EPI_SWIGLU); Y must be NULL.
+ * epilogue_flags DQ_EPI_SWIGLU: W rows are interleaved gate/up in groups of
+ *   16 (rows 32j..32j+15 = gate rows 16j.., rows 32j+16..32j+31 = up rows
+ *   16j..); the output column j = silu(gate_j) * up_j, N/2 columns.
+ * K % 16 == 0, M >= 0, N >= 0. */
+dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G_x_static,
+                          const dq_nvfp4_t* W, int64_t M, int out_kind, void* Y,
+                          const float* G_out_static, const dq_nvfp4_t* Yq, int epilogue_flags,
+                          void* stream);
+
+/* ---- a6: weight-only LUT GEMV (decode; no activation quantization) -------
+ * y[b, n] = sum_k x[b, k] * w_hat[n, k], fp32 accumulation.
+ * x: device bf16 [B, K] row-major, 1 <= B <= 16.  W: packed LUT weight.
+ * out_kind DQ_OUT_F32 / DQ_OUT_BF16: y is device [B, N] row-major.
+ * Activations are converted to fp16 inside the kernel after a per-row
+ * power-of-two rescale (exact for every bf16 value within 2^40 of the row's
+ * largest magnitude); products with the fp16 table are exact.  In PAPER_GRID
+ * mode the block scale is folded into the fp16 operand (one rounding,
+ * relative 2^-11 per weight). */
+dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y,
+                         void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DQ_H */

@@ -1,0 +1,242 @@
+// C ABI of libdq (declared in include/dq.h): host-side argument validation,
+// size queries and dispatch to the kernel launchers.  Validation runs before
+// any HIP call, so rejected calls launch nothing.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "dq.h"
+#include "dq_internal.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+dq_status fail(dq_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+dq_status ok() {
+  g_last_error[0] = '\0';
+  return DQ_OK;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int64_t rup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+dq_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  if (e == hipErrorNotSupported) return fail(DQ_ERR_UNSUPPORTED, "%s: configuration not supported", what);
+  return fail(DQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+dq_status check_nvfp4(const dq_nvfp4_t* t, const char* name, int64_t rows, int64_t cols) {
+  if (t == nullptr) return fail(DQ_ERR_INVALID_ARG, "%s is NULL", name);
+  if (t->codes == nullptr || t->scales == nullptr || t->G == nullptr)
+    return fail(DQ_ERR_INVALID_ARG, "%s has a NULL buffer", name);
+  if (!aligned(t->codes, 16) || !aligned(t->scales, 16) || !aligned(t->G, 4))
+    return fail(DQ_ERR_INVALID_ARG, "%s buffers must be 16-byte aligned (G 4-byte)", name);
+  if (t->rows != rows || t->cols != cols)
+    return fail(DQ_ERR_INVALID_ARG, "%s is %lldx%lld, expected %lldx%lld", name, (long long)t->rows,
+                (long long)t->cols, (long long)rows, (long long)cols);
+  return DQ_OK;
+}
+
+dq::NvFp4View view(const dq_nvfp4_t* t) { return dq::NvFp4View{t->codes, t->scales, t->G, t->rows, t->cols}; }
+
+dq_status check_lut(const dq_lut_t* t, const char* name) {
+  if (t == nullptr) return fail(DQ_ERR_INVALID_ARG, "%s is NULL", name);
+  if (t->bits != 2 && t->bits != 3) return fail(DQ_ERR_INVALID_ARG, "%s.bits must be 2 or 3", name);
+  if (t->mode != DQ_LUT_PER_ROW && t->mode != DQ_LUT_PAPER_GRID)
+    return fail(DQ_ERR_INVALID_ARG, "%s.mode is not a DQ_LUT_* value", name);
+  if (t->rows < 0 || t->cols < 0 || t->cols % 32 != 0)
+    return fail(DQ_ERR_INVALID_ARG, "%s: rows >= 0 and cols %% 32 == 0 required", name);
+  if (t->codes == nullptr || t->lut == nullptr) return fail(DQ_ERR_INVALID_ARG, "%s has a NULL buffer", name);
+  if (!aligned(t->codes, 16) || !aligned(t->lut, 16))
+    return fail(DQ_ERR_INVALID_ARG, "%s buffers must be 16-byte aligned", name);
+  if (t->mode == DQ_LUT_PAPER_GRID) {
+    if (t->scales == nullptr || t->G == nullptr)
+      return fail(DQ_ERR_INVALID_ARG, "%s: PAPER_GRID needs scales and G", name);
+    if (!aligned(t->scales, 16) || !aligned(t->G, 4))
+      return fail(DQ_ERR_INVALID_ARG, "%s: scales must be 16-byte aligned, G 4-byte", name);
+  }
+  return DQ_OK;
+}
+
+dq::LutView view(const dq_lut_t* t) {
+  return dq::LutView{t->codes, t->lut, t->scales, t->G, t->rows, t->cols, t->bits, t->mode};
+}
+
+double f16_value(uint16_t h) {
+  const int e = (h >> 10) & 0x1F, m = h & 0x3FF;
+  double v = e == 0 ? m * (1.0 / (1 << 24)) : (1.0 + m / 1024.0) * (double)(1ll << e) / (double)(1 << 15);
+  return (h & 0x8000) ? -v : v;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dq_abi_version(void) { return DQ_ABI_VERSION; }
+
+const char* dq_status_string(dq_status s) {
+  switch (s) {
+    case DQ_OK: return "DQ_OK";
+    case DQ_ERR_INVALID_ARG: return "DQ_ERR_INVALID_ARG";
+    case DQ_ERR_UNSUPPORTED: return "DQ_ERR_UNSUPPORTED";
+    case DQ_ERR_HIP: return "DQ_ERR_HIP";
+    default: return "DQ_ERR_UNKNOWN";
+  }
+}
+
+const char* dq_last_error(void) { return g_last_error; }
+
+dq_status dq_nvfp4_sizes(int64_t rows, int64_t cols, size_t* code_bytes, size_t* scale_bytes) {
+  if (code_bytes == nullptr || scale_bytes == nullptr) return fail(DQ_ERR_INVALID_ARG, "NULL output pointer");
+  if (rows < 0 || cols < 0 || cols % 16 != 0)
+    return fail(DQ_ERR_INVALID_ARG, "rows >= 0, cols >= 0 and cols %% 16 == 0 required");
+  const int64_t r = rup(rows, 32), c = rup(cols, 64);
+  *code_bytes = (size_t)(r * c / 2);
+  *scale_bytes = (size_t)(r * c / 16);
+  return ok();
+}
+
+dq_status dq_lut_sizes(int bits, int mode, int64_t rows, int64_t cols, size_t* code_bytes, size_t* lut_bytes,
+                       size_t* scale_bytes) {
+  if (code_bytes == nullptr || lut_bytes == nullptr || scale_bytes == nullptr)
+    return fail(DQ_ERR_INVALID_ARG, "NULL output pointer");
+  if (bits != 2 && bits != 3) return fail(DQ_ERR_INVALID_ARG, "bits must be 2 or 3");
+  if (mode != DQ_LUT_PER_ROW && mode != DQ_LUT_PAPER_GRID) return fail(DQ_ERR_INVALID_ARG, "bad LUT mode");
+  if (rows < 0 || cols < 0 || cols % 32 != 0)
+    return fail(DQ_ERR_INVALID_ARG, "rows >= 0, cols >= 0 and cols %% 32 == 0 required");
+  const int64_t tr = rup(rows, 16) / 16, tc = rup(cols, 128) / 128;
+  const int64_t gb = bits == 3 ? 12 : 8;
+  *code_bytes = (size_t)(tr * tc * 64 * gb);
+  if (mode == DQ_LUT_PER_ROW) {
+    *lut_bytes = (size_t)(tr * 16 * (1 << bits) * 2);
+    *scale_bytes = 0;
+  } else {
+    *lut_bytes = (size_t)((1 << bits) * 2);
+    *scale_bytes = (size_t)(tr * tc * 128);
+  }
+  return ok();
+}
+
+dq_status dq_pack_nvfp4(const float* W, int64_t N, int64_t K, const float* G_override, const dq_nvfp4_t* out,
+                        void* stream) {
+  if (W == nullptr && N * K > 0) return fail(DQ_ERR_INVALID_ARG, "W is NULL");
+  if (!aligned(W, 16)) return fail(DQ_ERR_INVALID_ARG, "W must be 16-byte aligned");
+  if (N < 0 || K < 0 || K % 16 != 0) return fail(DQ_ERR_INVALID_ARG, "N >= 0, K >= 0, K %% 16 == 0 required");
+  if (G_override != nullptr && !aligned(G_override, 4)) return fail(DQ_ERR_INVALID_ARG, "G_override misaligned");
+  dq_status st = check_nvfp4(out, "out", N, K);
+  if (st != DQ_OK) return st;
+  return hip_status(dq::launch_pack_nvfp4(W, N, K, G_override, view(out), (hipStream_t)stream), "dq_pack_nvfp4");
+}
+
+dq_status dq_pack_lut3(const float* W, int64_t N, int64_t K, int bits, int mode, const uint16_t* grid,
+                       const dq_lut_t* out, void* stream) {
+  if (W == nullptr && N * K > 0) return fail(DQ_ERR_INVALID_ARG, "W is NULL");
+  if (!aligned(W, 16)) return fail(DQ_ERR_INVALID_ARG, "W must be 16-byte aligned");
+  if (N < 0 || K < 0 || K % 32 != 0) return fail(DQ_ERR_INVALID_ARG, "N >= 0, K >= 0, K %% 32 == 0 required");
+  if (bits != 2 && bits != 3) return fail(DQ_ERR_INVALID_ARG, "bits must be 2 or 3");
+  if (mode != DQ_LUT_PER_ROW && mode != DQ_LUT_PAPER_GRID) return fail(DQ_ERR_INVALID_ARG, "bad LUT mode");
+  dq_status st = check_lut(out, "out");
+  if (st != DQ_OK) return st;
+  if (out->rows != N || out->cols != K || out->bits != bits || out->mode != mode)
+    return fail(DQ_ERR_INVALID_ARG, "out descriptor does not match N, K, bits, mode");
+  if (mode == DQ_LUT_PER_ROW && K > 32768)
+    return fail(DQ_ERR_UNSUPPORTED, "PER_ROW packing sorts a row in LDS: K <= 32768");
+  if (mode == DQ_LUT_PER_ROW && K == 0 && N > 0)
+    return fail(DQ_ERR_INVALID_ARG, "PER_ROW needs K > 0 (bin means of empty rows are undefined)");
+  if (mode == DQ_LUT_PAPER_GRID && grid != nullptr) {
+    int zeros = 0;
+    for (int i = 0; i < (1 << bits); ++i) {
+      if ((grid[i] & 0x7FFF) == 0) ++zeros;
+      if ((grid[i] & 0x7C00) == 0x7C00) return fail(DQ_ERR_INVALID_ARG, "grid must be finite");
+      if (i > 0 && !(f16_value(grid[i]) > f16_value(grid[i - 1])))
+        return fail(DQ_ERR_INVALID_ARG, "grid must be strictly ascending");
+    }
+    if (zeros != 1) return fail(DQ_ERR_INVALID_ARG, "grid must contain exactly one zero level");
+  }
+  return hip_status(dq::launch_pack_lut(W, N, K, grid, view(out), (hipStream_t)stream), "dq_pack_lut3");
+}
+
+dq_status dq_quantize_act_nvfp4(const uint16_t* X, int64_t M, int64_t K, const float* G_static,
+                                const dq_nvfp4_t* out, void* stream) {
+  if (X == nullptr && M * K > 0) return fail(DQ_ERR_INVALID_ARG, "X is NULL");
+  if (!aligned(X, 16)) return fail(DQ_ERR_INVALID_ARG, "X must be 16-byte aligned");
+  if (M < 0 || K < 0 || K % 16 != 0) return fail(DQ_ERR_INVALID_ARG, "M >= 0, K >= 0, K %% 16 == 0 required");
+  if (G_static != nullptr && !aligned(G_static, 4)) return fail(DQ_ERR_INVALID_ARG, "G_static misaligned");
+  dq_status st = check_nvfp4(out, "out", M, K);
+  if (st != DQ_OK) return st;
+  return hip_status(dq::launch_quantize_act(X, M, K, G_static, view(out), (hipStream_t)stream),
+                    "dq_quantize_act_nvfp4");
+}
+
+dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G_x_static, const dq_nvfp4_t* W,
+                          int64_t M, int out_kind, void* Y, const float* G_out_static, const dq_nvfp4_t* Yq,
+                          int epilogue_flags, void* stream) {
+  if ((A == nullptr) == (X == nullptr)) return fail(DQ_ERR_INVALID_ARG, "give exactly one of A and X");
+  if (W == nullptr) return fail(DQ_ERR_INVALID_ARG, "W is NULL");
+  if (M < 0) return fail(DQ_ERR_INVALID_ARG, "M < 0");
+  const int64_t N = W->rows, K = W->cols;
+  dq_status st = check_nvfp4(W, "W", N, K);
+  if (st != DQ_OK) return st;
+  if (N < 0 || K < 0 || K % 16 != 0) return fail(DQ_ERR_INVALID_ARG, "W: rows >= 0 and cols %% 16 == 0 required");
+  if (A != nullptr) {
+    st = check_nvfp4(A, "A", M, K);
+    if (st != DQ_OK) return st;
+  } else {
+    if (G_x_static == nullptr || !aligned(G_x_static, 4))
+      return fail(DQ_ERR_INVALID_ARG, "the fused path needs an aligned G_x_static");
+    if (!aligned(X, 16)) return fail(DQ_ERR_INVALID_ARG, "X must be 16-byte aligned");
+  }
+  if (epilogue_flags & ~DQ_EPI_SWIGLU) return fail(DQ_ERR_INVALID_ARG, "unknown epilogue flag");
+  if (out_kind != DQ_OUT_F32 && out_kind != DQ_OUT_BF16 && out_kind != DQ_OUT_NVFP4)
+    return fail(DQ_ERR_INVALID_ARG, "bad out_kind");
+  if (out_kind == DQ_OUT_NVFP4) {
+    if (Y != nullptr) return fail(DQ_ERR_INVALID_ARG, "NVFP4 output: Y must be NULL");
+    if (G_out_static == nullptr || !aligned(G_out_static, 4))
+      return fail(DQ_ERR_INVALID_ARG, "NVFP4 output needs an aligned G_out_static");
+  } else {
+    if (Y == nullptr && M * N > 0) return fail(DQ_ERR_INVALID_ARG, "Y is NULL");
+    if (!aligned(Y, 16)) return fail(DQ_ERR_INVALID_ARG, "Y must be 16-byte aligned");
+  }
+  if (X != nullptr) return fail(DQ_ERR_UNSUPPORTED, "fused activation quantization is not built yet");
+  if (out_kind == DQ_OUT_NVFP4 || epilogue_flags != 0)
+    return fail(DQ_ERR_UNSUPPORTED, "NVFP4 / SwiGLU epilogues are not built yet");
+  dq::GemmArgs a{};
+  if (A) a.A = view(A);
+  a.X = X;
+  a.G_x = G_x_static;
+  a.W = view(W);
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.out_kind = out_kind;
+  a.Y = Y;
+  a.G_out = G_out_static;
+  if (Yq) a.Yq = view(Yq);
+  a.flags = epilogue_flags;
+  return hip_status(dq::launch_gemm(a, (hipStream_t)stream), "dq_prefill_gemm");
+}
+
+dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y, void* stream) {
+  dq_status st = check_lut(W, "W");
+  if (st != DQ_OK) return st;
+  if (B < 1 || B > 16) return fail(DQ_ERR_INVALID_ARG, "1 <= B <= 16 required");
+  if (x == nullptr || !aligned(x, 16)) return fail(DQ_ERR_INVALID_ARG, "x must be non-NULL and 16-byte aligned");
+  if (out_kind != DQ_OUT_F32 && out_kind != DQ_OUT_BF16) return fail(DQ_ERR_INVALID_ARG, "bad out_kind");
+  if (y == nullptr && W->rows > 0) return fail(DQ_ERR_INVALID_ARG, "y is NULL");
+  if (!aligned(y, 16)) return fail(DQ_ERR_INVALID_ARG, "y must be 16-byte aligned");
+  return hip_status(dq::launch_gemv(x, B, view(W), out_kind, y, (hipStream_t)stream), "dq_decode_gemv");
+}
+
+}  // extern "C"

@@ -1,0 +1,55 @@
+// Internal launcher interface between the C ABI (dq_api.cpp) and the kernel
+// translation units.  Views carry validated device pointers and logical sizes.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dq {
+
+struct NvFp4View {
+  uint8_t* codes;
+  uint8_t* scales;
+  float* G;
+  int64_t rows, cols;
+};
+
+struct LutView {
+  uint8_t* codes;
+  uint16_t* lut;
+  uint8_t* scales;
+  float* G;
+  int64_t rows, cols;
+  int bits, mode;
+};
+
+// a1 / a2: NVFP4 quantization (quant.hip)
+hipError_t launch_quantize_act(const uint16_t* X, int64_t M, int64_t K, const float* G_static,
+                               const NvFp4View& out, hipStream_t s);
+hipError_t launch_pack_nvfp4(const float* W, int64_t N, int64_t K, const float* G_override,
+                             const NvFp4View& out, hipStream_t s);
+
+// a5: LUT packing (pack_lut.hip)
+hipError_t launch_pack_lut(const float* W, int64_t N, int64_t K, const uint16_t* grid_host,
+                           const LutView& out, hipStream_t s);
+
+// a3 / a4: NVFP4 GEMM (gemm.hip)
+struct GemmArgs {
+  NvFp4View A;            // valid when X == nullptr
+  const uint16_t* X;      // fused activation quantization input, or nullptr
+  const float* G_x;       // static activation scale for the fused path
+  NvFp4View W;
+  int64_t M, N, K;
+  int out_kind;
+  void* Y;
+  const float* G_out;     // static output scale (NVFP4 output)
+  NvFp4View Yq;
+  int flags;
+};
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
+
+// a6: LUT GEMV (gemv.hip)
+hipError_t launch_gemv(const uint16_t* x, int64_t B, const LutView& w, int out_kind, void* y,
+                       hipStream_t s);
+
+}  // namespace dq

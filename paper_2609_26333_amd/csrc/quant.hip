@@ -1,0 +1,210 @@
+// NVFP4 quantization kernels (paper App. A, "NVFP4-esque two-level scaling"
+// and "NVFP4"): the activation quantizer (bf16 input, static or dynamic
+// global scale) and the weight packer (fp32 input, round to nearest).
+//
+// Both are HBM-bound streaming kernels.  One wavefront owns one 32-row x
+// 64-column tile of the tiled NVFP4 layout (dq.h): it reads 32 rows of 64
+// elements with fully coalesced 16-byte loads (8 lanes per row), computes the
+// per-16 block maxima with one cross-lane exchange, and writes the 1 KiB code
+// tile and 128-byte scale tile with contiguous stores.
+#include "dq_device.hpp"
+#include "dq_internal.hpp"
+
+namespace dq {
+
+// ------------------------------------------------------------ global amax
+__global__ void zero_float_kernel(float* p) { *p = 0.0f; }
+
+__global__ void finalize_global_scale_kernel(float* p) {
+  float a = *p;
+  *p = (a == 0.0f) ? 1.0f : a / kGlobalDivisor;
+}
+
+__global__ void copy_float_kernel(const float* src, float* dst) { *dst = *src; }
+
+template <typename T>
+__global__ __launch_bounds__(256) void amax_kernel(const T* __restrict__ x, int64_t n_vec,
+                                                   int64_t n, float* out);
+
+// bf16: 8 elements per 16-byte vector
+template <>
+__global__ __launch_bounds__(256) void amax_kernel<uint16_t>(const uint16_t* __restrict__ x,
+                                                             int64_t n_vec, int64_t n, float* out) {
+  float m = 0.0f;
+  const uint4_t* xv = reinterpret_cast<const uint4_t*>(x);
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n_vec;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    uint4_t v = __builtin_nontemporal_load(&xv[i]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      m = fmaxf(m, fabsf(bf16_lo(v[j])));
+      m = fmaxf(m, fabsf(bf16_hi(v[j])));
+    }
+  }
+  // tail (n not a multiple of 8)
+  for (int64_t i = n_vec * 8 + blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    m = fmaxf(m, fabsf(__uint_as_float((uint32_t)x[i] << 16)));
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) atomic_max_nonneg(out, m);
+}
+
+// fp32: 4 elements per 16-byte vector
+template <>
+__global__ __launch_bounds__(256) void amax_kernel<float>(const float* __restrict__ x, int64_t n_vec,
+                                                          int64_t n, float* out) {
+  float m = 0.0f;
+  const float4_t* xv = reinterpret_cast<const float4_t*>(x);
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n_vec;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    float4_t v = __builtin_nontemporal_load(&xv[i]);
+    m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+  }
+  for (int64_t i = n_vec * 4 + blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    m = fmaxf(m, fabsf(x[i]));
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) atomic_max_nonneg(out, m);
+}
+
+// ------------------------------------------------------------ tile quantizer
+// Loads 8 consecutive elements of one row as fp32 (zeros when out of range).
+__device__ inline void load8(const uint16_t* __restrict__ x, int64_t ld, int64_t row, int64_t col,
+                             bool ok, float (&v)[8]) {
+  if (ok) {
+    uint4_t w = *reinterpret_cast<const uint4_t*>(x + row * ld + col);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[2 * j] = bf16_lo(w[j]);
+      v[2 * j + 1] = bf16_hi(w[j]);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = 0.0f;
+  }
+}
+
+__device__ inline void load8(const float* __restrict__ x, int64_t ld, int64_t row, int64_t col,
+                             bool ok, float (&v)[8]) {
+  if (ok) {
+    const float4_t* p = reinterpret_cast<const float4_t*>(x + row * ld + col);
+    float4_t a = p[0], b = p[1];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[j] = a[j];
+      v[4 + j] = b[j];
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = 0.0f;
+  }
+}
+
+// Quantize 8 values of a 16-block whose other half lives in lane ^ 1.
+// Returns the 4 code bytes (element 2j low nibble of byte j) and the scale.
+__device__ inline uint32_t quantize8(const float (&v)[8], float G, uint32_t& scale_code) {
+  float a = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) a = fmaxf(a, fabsf(v[j]));
+  a = fmaxf(a, __shfl_xor(a, 1, 64));
+  const float den = 6.0f * G;
+  const float t = a / den;                       // correctly rounded division
+  const uint32_t c = e4m3_encode_rne_sat(t);
+  const float S = e4m3_decode(c) * G;
+  scale_code = c;
+  if (S == 0.0f) return 0u;
+  const float rcp = 1.0f / S;
+  uint32_t w = 0;
+  w = cvt_pk_fp4<0>(w, div_by_scale(v[0], S, rcp), div_by_scale(v[1], S, rcp));
+  w = cvt_pk_fp4<1>(w, div_by_scale(v[2], S, rcp), div_by_scale(v[3], S, rcp));
+  w = cvt_pk_fp4<2>(w, div_by_scale(v[4], S, rcp), div_by_scale(v[5], S, rcp));
+  w = cvt_pk_fp4<3>(w, div_by_scale(v[6], S, rcp), div_by_scale(v[7], S, rcp));
+  return fp4_canonical_zero(w);
+}
+
+// One wavefront per 32x64 tile; 4 wavefronts per block.
+template <typename T>
+__global__ __launch_bounds__(256) void quantize_tiles_kernel(const T* __restrict__ x, int64_t rows,
+                                                             int64_t cols, const float* __restrict__ Gp,
+                                                             uint8_t* __restrict__ codes,
+                                                             uint8_t* __restrict__ scales,
+                                                             int64_t tiles_r, int64_t tiles_c,
+                                                             float* G_out) {
+  const int lane = threadIdx.x & 63;
+  const int64_t tile = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const float G = *Gp;
+  if (tile == 0 && lane == 0 && G_out != nullptr) *G_out = G;
+  if (tile >= tiles_r * tiles_c) return;
+  const int64_t tr = tile / tiles_c, tc = tile % tiles_c;
+  const int c = lane & 7;
+  const int64_t col = tc * 64 + c * 8;
+  const bool col_ok = col < cols;
+  uint32_t* code_tile = reinterpret_cast<uint32_t*>(codes + tile * 1024);
+  uint8_t* scale_tile = scales + tile * 128;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 8 * i + (lane >> 3);
+    const int64_t row = tr * 32 + r;
+    float v[8];
+    load8(x, cols, row, col, col_ok && row < rows, v);
+    uint32_t sc;
+    const uint32_t w = quantize8(v, G, sc);
+    code_tile[r * 8 + c] = w;
+    if ((c & 1) == 0) scale_tile[r * 4 + (c >> 1)] = (uint8_t)sc;
+  }
+}
+
+// ------------------------------------------------------------ launchers
+static int grid_for(int64_t n_vec) {
+  int64_t b = (n_vec + 255) / 256;
+  if (b > 4096) b = 4096;
+  if (b < 1) b = 1;
+  return (int)b;
+}
+
+template <typename T>
+static hipError_t launch_amax(const T* x, int64_t n, float* out, hipStream_t s) {
+  const int64_t per_vec = 16 / sizeof(T);
+  const int64_t n_vec = n / per_vec;
+  hipLaunchKernelGGL(zero_float_kernel, dim3(1), dim3(1), 0, s, out);
+  hipLaunchKernelGGL(amax_kernel<T>, dim3(grid_for(n_vec)), dim3(256), 0, s, x, n_vec, n, out);
+  hipLaunchKernelGGL(finalize_global_scale_kernel, dim3(1), dim3(1), 0, s, out);
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_quantize(const T* x, int64_t rows, int64_t cols, const float* Gp,
+                                  const NvFp4View& out, hipStream_t s) {
+  const int64_t tiles_r = round_up(rows, 32) / 32, tiles_c = round_up(cols, 64) / 64;
+  const int64_t tiles = tiles_r * tiles_c;
+  if (tiles == 0) {
+    if (Gp != out.G) hipLaunchKernelGGL(copy_float_kernel, dim3(1), dim3(1), 0, s, Gp, out.G);
+    return hipGetLastError();
+  }
+  const int64_t blocks = (tiles + 3) / 4;
+  hipLaunchKernelGGL(quantize_tiles_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, x, rows, cols,
+                     Gp, out.codes, out.scales, tiles_r, tiles_c, Gp == out.G ? nullptr : out.G);
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize_act(const uint16_t* X, int64_t M, int64_t K, const float* G_static,
+                               const NvFp4View& out, hipStream_t s) {
+  if (G_static == nullptr) {
+    hipError_t e = launch_amax(X, M * K, out.G, s);
+    if (e != hipSuccess) return e;
+    return launch_quantize(X, M, K, out.G, out, s);
+  }
+  return launch_quantize(X, M, K, G_static, out, s);
+}
+
+hipError_t launch_pack_nvfp4(const float* W, int64_t N, int64_t K, const float* G_override,
+                             const NvFp4View& out, hipStream_t s) {
+  if (G_override == nullptr) {
+    hipError_t e = launch_amax(W, N * K, out.G, s);
+    if (e != hipSuccess) return e;
+    return launch_quantize(W, N, K, out.G, out, s);
+  }
+  return launch_quantize(W, N, K, G_override, out, s);
+}
+
+}  // namespace dq

@@ -1,0 +1,117 @@
+"""C-ABI contract checks that need no GPU: the library loads, exports every
+function include/dq.h declares, and rejects invalid arguments on the host
+before any HIP call (DQ_ERR_INVALID_ARG / DQ_ERR_UNSUPPORTED)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_26333_amd as dq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "dq.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dq_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared()
+    assert len(names) >= 10
+    lib = ctypes.CDLL(dq.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(dq.EXPORTED)
+
+
+def test_version_and_status_strings():
+    assert dq.abi_version() == 1
+    lib = dq.lib()
+    assert lib.dq_status_string(0) == b"DQ_OK"
+    assert lib.dq_status_string(-1) == b"DQ_ERR_INVALID_ARG"
+    assert lib.dq_status_string(-2) == b"DQ_ERR_UNSUPPORTED"
+    assert lib.dq_status_string(-3) == b"DQ_ERR_HIP"
+
+
+def test_size_queries():
+    assert dq.nvfp4_sizes(100, 48) == (128 * 64 // 2, 128 * 64 // 16)
+    assert dq.nvfp4_sizes(0, 0) == (0, 0)
+    assert dq.lut_sizes(3, dq.LUT_PER_ROW, 20, 96) == (2 * 1 * 64 * 12, 32 * 8 * 2, 0)
+    assert dq.lut_sizes(2, dq.LUT_PAPER_GRID, 16, 256) == (1 * 2 * 64 * 8, 8, 2 * 128)
+    with pytest.raises(dq.DQError) as e:
+        dq.nvfp4_sizes(4, 24)
+    assert e.value.status == dq.DQ_ERR_INVALID_ARG
+    with pytest.raises(dq.DQError):
+        dq.lut_sizes(4, 0, 16, 32)
+    with pytest.raises(dq.DQError):
+        dq.lut_sizes(3, 0, 16, 48)
+
+
+def _nv(rows, cols, codes=16, scales=16, G=16):
+    return dq._NvFp4(codes, scales, G, rows, cols)
+
+
+def test_invalid_arguments_rejected_on_host():
+    lib = dq.lib()
+    fake = 1 << 20                       # never dereferenced: validation fails first
+    d = _nv(4, 24, fake, fake, fake)
+    # K % 16 != 0
+    assert lib.dq_quantize_act_nvfp4(fake, 4, 24, None, ctypes.byref(d), None) == dq.DQ_ERR_INVALID_ARG
+    assert b"16" in lib.dq_last_error()
+    # misaligned input
+    d = _nv(4, 32, fake, fake, fake)
+    assert lib.dq_quantize_act_nvfp4(fake + 2, 4, 32, None, ctypes.byref(d), None) == dq.DQ_ERR_INVALID_ARG
+    # descriptor shape mismatch
+    d = _nv(5, 32, fake, fake, fake)
+    assert lib.dq_pack_nvfp4(fake, 4, 32, None, ctypes.byref(d), None) == dq.DQ_ERR_INVALID_ARG
+    # NULL descriptor buffer
+    d = _nv(4, 32, fake, 0, fake)
+    assert lib.dq_pack_nvfp4(fake, 4, 32, None, ctypes.byref(d), None) == dq.DQ_ERR_INVALID_ARG
+    # GEMM: both A and X / neither
+    a = _nv(4, 32, fake, fake, fake)
+    w = _nv(8, 32, fake, fake, fake)
+    assert lib.dq_prefill_gemm(ctypes.byref(a), fake, fake, ctypes.byref(w), 4, 0, fake, None, None, 0,
+                               None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_prefill_gemm(None, None, None, ctypes.byref(w), 4, 0, fake, None, None, 0,
+                               None) == dq.DQ_ERR_INVALID_ARG
+    # GEMM: K mismatch between A and W
+    a2 = _nv(4, 48, fake, fake, fake)
+    assert lib.dq_prefill_gemm(ctypes.byref(a2), None, None, ctypes.byref(w), 4, 0, fake, None, None, 0,
+                               None) == dq.DQ_ERR_INVALID_ARG
+    # GEMM: bad out kind, bad flag
+    assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w), 4, 7, fake, None, None, 0,
+                               None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w), 4, 0, fake, None, None, 4,
+                               None) == dq.DQ_ERR_INVALID_ARG
+    # GEMV: batch out of range, bad bits
+    lw = dq._Lut(fake, fake, None, None, 16, 128, 3, 0)
+    assert lib.dq_decode_gemv(fake, 0, ctypes.byref(lw), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_decode_gemv(fake, 17, ctypes.byref(lw), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
+    lw_bad = dq._Lut(fake, fake, None, None, 16, 128, 4, 0)
+    assert lib.dq_decode_gemv(fake, 1, ctypes.byref(lw_bad), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
+    # PAPER_GRID without scales / G
+    lw_p = dq._Lut(fake, fake, None, None, 16, 128, 3, 1)
+    assert lib.dq_decode_gemv(fake, 1, ctypes.byref(lw_p), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
+    # LUT pack: K % 32, PER_ROW K limit, bad grid
+    lo = dq._Lut(fake, fake, None, None, 16, 48, 3, 0)
+    assert lib.dq_pack_lut3(fake, 16, 48, 3, 0, None, ctypes.byref(lo), None) == dq.DQ_ERR_INVALID_ARG
+    lo = dq._Lut(fake, fake, None, None, 16, 65536, 3, 0)
+    assert lib.dq_pack_lut3(fake, 16, 65536, 3, 0, None, ctypes.byref(lo), None) == dq.DQ_ERR_UNSUPPORTED
+    lp = dq._Lut(fake, fake, fake, fake, 16, 128, 2, 1)
+    bad_grid = (ctypes.c_uint16 * 4)(0x4000, 0x3C00, 0x0000, 0x4600)      # not ascending
+    assert lib.dq_pack_lut3(fake, 16, 128, 2, 1, bad_grid, ctypes.byref(lp), None) == dq.DQ_ERR_INVALID_ARG
+    no_zero = (ctypes.c_uint16 * 4)(0xC000, 0x3C00, 0x4000, 0x4600)
+    assert lib.dq_pack_lut3(fake, 16, 128, 2, 1, no_zero, ctypes.byref(lp), None) == dq.DQ_ERR_INVALID_ARG
+
+
+def test_oracle_is_not_imported_by_the_product():
+    """The binding and the C sources never reach into oracle/."""
+    pkg = os.path.join(ROOT, "paper_2609_26333_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".hpp", ".h")):
+                txt = open(os.path.join(dirpath, f)).read()
+                assert "import oracle" not in txt and "from oracle" not in txt, f

@@ -1,0 +1,294 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bars: codes, scales, LUT entries and global scales bit-exact; GEMM / GEMV
+fp32 outputs within 1e-3 relative Frobenius error of the fp64 oracle (bf16
+outputs against the oracle rounded to bf16).  Inputs are seeded synthetic
+tensors (synth/); no expected value comes from the GPU.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import dq_layout as L  # noqa: E402
+
+import synth  # noqa: E402
+from oracle import formats, linalg, lut, nvfp4  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-3
+
+try:
+    import paper_2609_26333_amd as dq
+except ImportError:  # pragma: no cover
+    dq = None
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if dq is None or not torch.cuda.is_available():
+        pytest.skip("needs the built HIP library and a GPU")
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def bf16_dev(bits):
+    return dev(np.asarray(bits, np.uint16).view(np.int16))
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+# ---------------------------------------------------------------- a1: activation quantization
+def _check_nvfp4(t, rows, cols, q_ref, c_ref, G_ref):
+    q, c, qfull, cfull = L.nvfp4_unpack(host(t.codes), host(t.scales), rows, cols)
+    assert np.array_equal(c, c_ref), f"scales differ at {np.argwhere(c != c_ref)[:5]}"
+    assert np.array_equal(q, q_ref), f"codes differ at {np.argwhere(q != q_ref)[:5]}"
+    # padding of the tiled layout holds zeros
+    assert not qfull[rows:].any() and not qfull[:, cols:].any()
+    assert not cfull[rows:].any() and not cfull[:, cols // 16:].any()
+    assert host(t.G)[0] == np.float32(G_ref)
+
+
+ACT_SHAPES = [(128, 512, 0), (100, 48, 1), (1, 16, 2), (33, 1040, 3), (2048, 4096, 5)]
+
+
+@pytest.mark.parametrize("M,K,seed", ACT_SHAPES)
+@pytest.mark.parametrize("static", [False, True])
+def test_act_quant(M, K, seed, static):
+    say("act_quant", M, K, seed, static)
+    xb = synth.random_bf16(seed, (M, K), outlier_frac=0.01, outlier_factor=20)
+    G_static = None
+    if static:
+        calib = synth.random_bf16(seed + 1000, (M, K), outlier_frac=0.01, outlier_factor=20)
+        G_static = nvfp4.global_scale(nvfp4.amax(formats.f32_from_bf16_bits(calib)))
+    q_ref, c_ref, G_ref = nvfp4.quantize_bf16_activations(xb, G_static)
+    Gd = dev(np.array([G_static], np.float32)) if static else None
+    t = dq.dq_quantize_act_nvfp4(bf16_dev(xb), G_static=Gd)
+    _check_nvfp4(t, M, K, q_ref, c_ref, G_ref)
+
+
+def test_act_quant_empty():
+    t = dq.dq_quantize_act_nvfp4(bf16_dev(np.zeros((0, 64), np.uint16)))
+    assert host(t.G)[0] == 1.0
+
+
+def test_act_quant_midpoints_and_saturation():
+    """Blocks whose elements sit exactly on E2M1 midpoints (and one bf16 ulp
+    either side) after division by the block scale, plus saturated blocks."""
+    rng = np.random.default_rng(7)
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0])
+    rows = []
+    for v in formats.E4M3_VALUES[8:126:3]:                # normal-range scales
+        blk = np.concatenate([[6.0], mids, -mids, [0.0]]) * v
+        rows.append(blk)
+    x = np.array(rows, np.float32)
+    xb = synth.bf16_bits_from_f32(x)
+    nz = (xb & 0x7FFF) != 0                   # perturb nonzero magnitudes by one bf16 ulp
+    up = np.where(nz, xb + 1, xb).astype(np.uint16)
+    dn = np.where(nz, xb - 1, xb).astype(np.uint16)
+    dn[:, 0] = xb[:, 0]
+    up[:, 0] = xb[:, 0]
+    sat = synth.bf16_bits_from_f32(np.float32(1e4) * rng.standard_normal((x.shape[0], 16)).astype(np.float32))
+    allx = np.concatenate([np.concatenate([xb, up, dn, sat], axis=1)] * 2, axis=0)
+    G = np.float32(1.0)
+    q_ref, c_ref, _ = nvfp4.quantize_bf16_activations(allx, G)
+    t = dq.dq_quantize_act_nvfp4(bf16_dev(allx), G_static=dev(np.array([G], np.float32)))
+    _check_nvfp4(t, allx.shape[0], allx.shape[1], q_ref, c_ref, G)
+
+
+# ---------------------------------------------------------------- a2: weight packing
+@pytest.mark.parametrize("N,K,seed", [(512, 512, 0), (72, 48, 1), (12288, 4096, 2)])
+def test_pack_nvfp4(N, K, seed):
+    say("pack_nvfp4", N, K)
+    w = synth.random_f32(seed, (N, K), 0.02)
+    w *= np.exp(0.3 * synth.random_f32(seed + 1, (N, 1))).astype(np.float32)
+    q_ref, c_ref, G_ref = nvfp4.quantize_dynamic(w)
+    t = dq.dq_pack_nvfp4(dev(w))
+    _check_nvfp4(t, N, K, q_ref, c_ref, G_ref)
+
+
+def test_pack_nvfp4_shared_scale_and_fp32_midpoints():
+    """A shared (overridden) global scale, and fp32 elements one ulp around
+    every E2M1 midpoint (exercises the exact division)."""
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0], np.float32)
+    rows = []
+    for v in formats.E4M3_VALUES[8:126:5].astype(np.float32):
+        base = np.concatenate([[6.0], mids, [-0.75, -5.0, 0.0, 1.0, 2.0, 3.0, 4.0, 0.5]]).astype(np.float32) * v
+        rows += [base, np.nextafter(base, np.float32(np.inf)), np.nextafter(base, np.float32(-np.inf))]
+    w = np.array(rows, np.float32)
+    w[1::3, 0] = w[0::3, 0]
+    w[2::3, 0] = w[0::3, 0]
+    G = np.float32(1.0)
+    q_ref, c_ref = nvfp4.quantize(w, G)
+    t = dq.dq_pack_nvfp4(dev(w), G_override=dev(np.array([G], np.float32)))
+    _check_nvfp4(t, w.shape[0], w.shape[1], q_ref, c_ref, G)
+
+
+# ---------------------------------------------------------------- a3: GEMM
+def _upload_nvfp4(q, c, G):
+    rows, cols = q.shape
+    t = dq.NvFp4Tensor.empty(rows, cols)
+    cb, sb = L.nvfp4_pack(q, c)
+    t.codes[: cb.size].copy_(dev(cb))
+    t.scales[: sb.size].copy_(dev(sb))
+    t.G.copy_(dev(np.array([G], np.float32)))
+    return t
+
+
+GEMM_SHAPES = [(128, 512, 512), (100, 72, 48), (1, 1, 16), (300, 520, 1024), (257, 33, 64), (64, 256, 4096)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+def test_gemm_oracle_operands(M, N, K):
+    """GEMM alone: operands quantized by the oracle, laid out on the host."""
+    say("gemm", M, N, K)
+    xb = synth.random_bf16(11, (M, K), outlier_frac=0.01, outlier_factor=20)
+    w = synth.random_f32(12, (N, K), 0.02)
+    qa, ca, Ga = nvfp4.quantize_bf16_activations(xb)
+    qw, cw, Gw = nvfp4.quantize_dynamic(w)
+    ref = linalg.nvfp4_gemm(qa, ca, Ga, qw, cw, Gw)
+    A, W = _upload_nvfp4(qa, ca, Ga), _upload_nvfp4(qw, cw, Gw)
+    y = host(dq.dq_prefill_gemm(W, A=A, out_kind=dq.OUT_F32))
+    err = linalg.rel_fro(y, ref)
+    say("  rel_fro", err)
+    assert err <= TOL
+    yb = dq.dq_prefill_gemm(W, A=A, out_kind=dq.OUT_BF16)
+    ybf = host(yb.float()).astype(np.float64)
+    assert linalg.rel_fro(ybf, formats.bf16_rne_from_f64(ref)) <= TOL
+
+
+def test_gemm_exact_unit_scales():
+    """Unit block scales and G = 1: every partial sum is a multiple of 1/4 and
+    small, so the fp32 result must equal the exact one."""
+    rng = np.random.default_rng(13)
+    M, N, K = 96, 160, 512
+    qa = rng.integers(0, 16, (M, K)).astype(np.uint8)
+    qw = rng.integers(0, 16, (N, K)).astype(np.uint8)
+    qa[qa == 8] = 0
+    qw[qw == 8] = 0
+    ones_a = np.full((M, K // 16), 0x38, np.uint8)
+    ones_w = np.full((N, K // 16), 0x38, np.uint8)
+    ref = linalg.nvfp4_gemm(qa, ones_a, 1.0, qw, ones_w, 1.0)
+    y = host(dq.dq_prefill_gemm(_upload_nvfp4(qw, ones_w, 1.0), A=_upload_nvfp4(qa, ones_a, 1.0)))
+    assert np.array_equal(y.astype(np.float64), ref)
+
+
+def test_gemm_end_to_end_c1_sampled_rows():
+    """The 8B up-projection at full size (M=2048, K=4096, N=12288) through the
+    GPU quantizers and GEMM in the benchmark's launch configuration; 48 rows
+    of the output checked against the oracle."""
+    cfg = synth.CONFIGS[1]
+    layer = cfg.layers[0]
+    w = synth.layer_weight(cfg, layer)
+    xb = synth.prefill_x(cfg, layer.k)
+    calib = synth.prefill_x(cfg, layer.k, calib=True)
+    G_x = nvfp4.global_scale(nvfp4.amax(formats.f32_from_bf16_bits(calib)))
+    W = dq.dq_pack_nvfp4(dev(w))
+    A = dq.dq_quantize_act_nvfp4(bf16_dev(xb), G_static=dev(np.array([G_x], np.float32)))
+    Y = dq.dq_prefill_gemm(W, A=A, out_kind=dq.OUT_BF16)
+    rows = np.sort(np.random.default_rng(14).choice(cfg.m, 48, replace=False))
+    qa, ca, _ = nvfp4.quantize_bf16_activations(xb[rows], G_x)
+    qw, cw, Gw = nvfp4.quantize_dynamic(w)
+    ref = linalg.nvfp4_gemm(qa, ca, G_x, qw, cw, Gw)
+    y = host(Y[torch.from_numpy(rows).cuda()].float()).astype(np.float64)
+    err = linalg.rel_fro(y, formats.bf16_rne_from_f64(ref))
+    say("  c1 sampled rel_fro", err)
+    assert err <= TOL
+
+
+def test_gemm_empty():
+    W = dq.dq_pack_nvfp4(dev(synth.random_f32(1, (32, 64))))
+    A = dq.dq_quantize_act_nvfp4(bf16_dev(np.zeros((0, 64), np.uint16)))
+    y = dq.dq_prefill_gemm(W, A=A)
+    assert y.shape == (0, 32)
+
+
+# ---------------------------------------------------------------- a5 + a6: LUT pack and GEMV
+def _lut_weight(N, K, seed):
+    w = synth.random_f32(seed, (N, K), 0.02)
+    return w * np.exp(0.3 * synth.random_f32(seed + 1, (N, 1))).astype(np.float32)
+
+
+LUT_CASES = [(512, 512, 1, 3), (20, 96, 1, 3), (20, 96, 3, 2), (48, 4096, 4, 2), (12288, 4096, 1, 3),
+             (12288, 4096, 4, 3), (64, 4096, 16, 3), (40, 17408, 16, 3), (5120, 17408, 1, 3)]
+
+
+@pytest.mark.parametrize("N,K,B,bits", LUT_CASES)
+def test_lut_per_row_pack_and_gemv(N, K, B, bits):
+    say("lut per_row", N, K, B, bits)
+    w = _lut_weight(N, K, 20 + bits)
+    codes_ref, lut_ref = lut.quantize_per_row(w, bits)
+    Wq = dq.dq_pack_lut3(dev(w), bits=bits, mode=dq.LUT_PER_ROW)
+    codes = L.lut_codes_unpack(host(Wq.codes), N, K, bits)
+    table = host(Wq.lut).view(np.uint16)[: N * (1 << bits)].reshape(N, 1 << bits)
+    assert np.array_equal(table, lut_ref.view(np.uint16)), "LUT entries differ"
+    assert np.array_equal(codes, codes_ref), f"codes differ at {np.argwhere(codes != codes_ref)[:5]}"
+    xb = synth.random_bf16(30 + B, (B, K), outlier_frac=0.005, outlier_factor=30)
+    ref = linalg.lut_gemv_per_row(xb, codes_ref, lut_ref)
+    y = host(dq.dq_decode_gemv(bf16_dev(xb), Wq, out_kind=dq.OUT_F32))
+    err = linalg.rel_fro(y, ref)
+    say("  gemv rel_fro", err)
+    assert err <= TOL
+    if K <= 4096:
+        yb = host(dq.dq_decode_gemv(bf16_dev(xb), Wq, out_kind=dq.OUT_BF16).float()).astype(np.float64)
+        assert linalg.rel_fro(yb, formats.bf16_rne_from_f64(ref)) <= TOL
+
+
+@pytest.mark.parametrize("N,K,B,bits", [(512, 512, 1, 3), (20, 96, 2, 3), (37, 1024, 1, 2), (256, 4096, 4, 3)])
+def test_lut_paper_grid_pack_and_gemv(N, K, B, bits):
+    say("lut paper", N, K, B, bits)
+    w = _lut_weight(N, K, 40 + bits)
+    w[min(3, N - 1), :16] = 0.0                                   # a zero block
+    grid = lut.default_grid(bits)
+    codes_ref, sb_ref, G_ref = lut.quantize_paper_grid(w, grid)
+    Wq = dq.dq_pack_lut3(dev(w), bits=bits, mode=dq.LUT_PAPER_GRID)
+    codes = L.lut_codes_unpack(host(Wq.codes), N, K, bits)
+    sb = L.lut_scales_unpack(host(Wq.scales), N, K)
+    assert host(Wq.G)[0] == G_ref
+    assert np.array_equal(host(Wq.lut).view(np.uint16)[: 1 << bits], grid.view(np.uint16))
+    assert np.array_equal(sb, sb_ref), f"scales differ at {np.argwhere(sb != sb_ref)[:5]}"
+    assert np.array_equal(codes, codes_ref), f"codes differ at {np.argwhere(codes != codes_ref)[:5]}"
+    xb = synth.random_bf16(50 + B, (B, K), outlier_frac=0.005, outlier_factor=30)
+    ref = linalg.lut_gemv_paper(xb, codes_ref, sb_ref, G_ref, grid)
+    y = host(dq.dq_decode_gemv(bf16_dev(xb), Wq))
+    err = linalg.rel_fro(y, ref)
+    say("  gemv rel_fro", err)
+    assert err <= TOL
+
+
+def test_lut_paper_grid_custom_grid():
+    grid = np.array([-3.0, -1.0, 0.0, 0.5, 1.0, 2.0, 4.0, 6.0], np.float16)
+    w = _lut_weight(32, 256, 60)
+    codes_ref, sb_ref, G_ref = lut.quantize_paper_grid(w, grid)
+    Wq = dq.dq_pack_lut3(dev(w), bits=3, mode=dq.LUT_PAPER_GRID, grid=grid)
+    assert np.array_equal(L.lut_codes_unpack(host(Wq.codes), 32, 256, 3), codes_ref)
+    assert np.array_equal(L.lut_scales_unpack(host(Wq.scales), 32, 256), sb_ref)
+
+
+def test_gemv_large_activations_rescaled():
+    """Activations far outside fp16 range are rescaled per slice by a power of two."""
+    N, K = 64, 1024
+    w = _lut_weight(N, K, 70)
+    codes_ref, lut_ref = lut.quantize_per_row(w, 3)
+    x = synth.random_f32(71, (2, K))
+    x[0] *= np.float32(1e6)
+    x[1] *= np.float32(1e-6)
+    xb = synth.bf16_bits_from_f32(x)
+    ref = linalg.lut_gemv_per_row(xb, codes_ref, lut_ref)
+    Wq = dq.dq_pack_lut3(dev(w), bits=3)
+    y = host(dq.dq_decode_gemv(bf16_dev(xb), Wq))
+    for b in range(2):
+        assert linalg.rel_fro(y[b], ref[b]) <= TOL
