@@ -1,0 +1,226 @@
+#!/usr/bin/env python3
+"""Benchmark of the phase-specific quantized linear layer on one MI355X.
+
+Workload: the 8B-scale MLP up-projection (Qwen3-8B shape: K = d_model = 4096,
+N = d_ffn x 3 = 12288), prefill M = 2048 tokens with 0.5 % outlier channels
+x30, decode batches 1 and 4; weights 0.02 N(0,1) with a log-normal row scale.
+Inputs are seeded synthetic tensors already resident in HBM.
+
+One step = the whole per-token hot path over one batch:
+  1. NVFP4 activation quantization of X [2048, 4096] (static global scale),
+  2. W4A4 NVFP4 GEMM -> bf16 Y [2048, 12288],
+  3. LUT3 decode GEMV at batch 1 and at batch 4 (fp32 y).
+Weight packing (NVFP4 and per-row LUT3) is offline and timed separately.
+
+The decode weights rotate over enough packed copies (>= 512 MiB) that every
+GEMV streams its weights from HBM rather than from the 256 MiB Infinity Cache;
+the activations X rotate over 16 copies for the same reason.
+
+Prints one JSON line.  `value` is the prefill linear throughput: 2*M*N*K over
+(quantization + GEMM) time.  Per-kernel durations come from HIP events
+recorded on the launch stream around every kernel of the timed steps.
+"""
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "NVFP4 prefill GEMM TFLOPS (%FP4 peak); LUT3 decode GEMV GB/s (%HBM peak)"
+PEAK_FP16_TFLOPS = 2500.0      # dense fp16/bf16 MFMA, MI355X
+PEAK_FP4_TFLOPS = 10100.0      # dense fp4 MFMA, MI355X
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--decode-bytes", type=int, default=768 << 20,
+                   help="total bytes of rotated decode weight copies")
+    return p.parse_args()
+
+
+def cpu_baseline(cfg, w, X, G_x, xd):
+    """Time the CPU oracle on a bounded sample of the same workload."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import linalg, lut, nvfp4
+    N_s = 4096                                   # first third of the output features
+    w_s = w[:N_s]
+    qw, cw, Gw = nvfp4.quantize_dynamic(w_s)     # offline packing, not timed
+    codes, table = lut.quantize_per_row(w_s, 3)  # offline packing, not timed
+    t0 = time.perf_counter()
+    qa, ca, _ = nvfp4.quantize_bf16_activations(X, G_x)
+    Y = linalg.gemm(nvfp4.dequantize(qa, ca, G_x), nvfp4.dequantize(qw, cw, Gw))
+    t_pre = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    y = linalg.lut_gemv_per_row(xd, codes, table)
+    t_dec = time.perf_counter() - t0
+    M, K = X.shape
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    dec_bytes = N_s * K * 3 / 8 + N_s * 16 + xd.size * 2 + y.size * 4
+    del Y
+    return {
+        "value": 2.0 * M * N_s * K / t_pre / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+        "sample": (f"prefill: NVFP4 quantization of X[{M},{K}] + fp64 GEMM against the first {N_s} of "
+                   f"{w.shape[0]} weight rows ({t_pre:.2f} s); decode: LUT3 dequantization + fp64 GEMV "
+                   f"of those rows at batch 1 ({t_dec:.2f} s, {dec_bytes / t_dec / 1e9:.3f} GB/s); "
+                   f"weight packing untimed"),
+        "decode_gbps": dec_bytes / t_dec / 1e9,
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              f"(the sharded design is described in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2609_26333_amd as dq
+    import synth
+
+    torch.cuda.set_device(0)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()   # noqa: E731
+    cfg = synth.CONFIGS[1]
+    layer = cfg.layers[0]
+    M, N, K = cfg.m, layer.n, layer.k
+    Bs = cfg.decode_batches
+
+    w = synth.layer_weight(cfg, layer)
+    X = synth.prefill_x(cfg, K)
+    calib = synth.prefill_x(cfg, K, calib=True)
+    xds = {b: synth.decode_x(cfg, K, b) for b in Bs}
+
+    W_dev = dev(w)
+    s = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    Wq = dq.dq_pack_nvfp4(W_dev)
+    e1.record()
+    torch.cuda.synchronize()
+    t_pack_nvfp4 = e0.elapsed_time(e1)
+    e0.record()
+    Wl = dq.dq_pack_lut3(W_dev, bits=3, mode=dq.LUT_PER_ROW)
+    e1.record()
+    torch.cuda.synchronize()
+    t_pack_lut = e0.elapsed_time(e1)
+
+    # static activation scale from a calibration batch (running-max observer stand-in)
+    A_cal = dq.dq_quantize_act_nvfp4(dev(calib.view(np.int16)))
+    G_x = A_cal.G.clone()
+    torch.cuda.synchronize()
+    G_x_host = float(G_x.cpu()[0])
+
+    # rotation buffers
+    n_x = 16
+    Xs = [dev(X.view(np.int16)) for _ in range(n_x)]
+    lut_bytes = Wl.codes.numel() + Wl.lut.numel() * 2
+    n_w = max(2, -(-args.decode_bytes // lut_bytes))
+    Wls = [Wl] + [dq.LutWeight(Wl.codes.clone(), Wl.lut.clone(), None, None, N, K, 3, dq.LUT_PER_ROW)
+                  for _ in range(n_w - 1)]
+    xd_dev = {b: dev(xds[b].view(np.int16)) for b in Bs}
+    A = dq.NvFp4Tensor.empty(M, K)
+    Y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    ys = {b: torch.empty((b, N), dtype=torch.float32, device="cuda") for b in Bs}
+
+    # prebuilt raw C-ABI calls (keeps host enqueue far ahead of the GPU)
+    lib = dq.lib()
+    sp = ctypes.c_void_p(s.cuda_stream)
+    dA, dW = A.desc(), Wq.desc()
+    dWls = [x.desc() for x in Wls]
+    gx = ctypes.c_void_p(G_x.data_ptr())
+
+    def quant(i):
+        return lib.dq_quantize_act_nvfp4(ctypes.c_void_p(Xs[i % n_x].data_ptr()), M, K, gx, ctypes.byref(dA), sp)
+
+    def gemm():
+        return lib.dq_prefill_gemm(ctypes.byref(dA), None, None, ctypes.byref(dW), M, dq.OUT_BF16,
+                                   ctypes.c_void_p(Y.data_ptr()), None, None, 0, sp)
+
+    def gemv(i, b):
+        return lib.dq_decode_gemv(ctypes.c_void_p(xd_dev[b].data_ptr()), b, ctypes.byref(dWls[i % n_w]),
+                                  dq.OUT_F32, ctypes.c_void_p(ys[b].data_ptr()), sp)
+
+    names = ["quant", "gemm"] + [f"gemv_b{b}" for b in Bs]
+
+    def step(i, evs):
+        if evs:
+            evs[0].record(s)
+        assert quant(i) == 0
+        if evs:
+            evs[1].record(s)
+        assert gemm() == 0
+        if evs:
+            evs[2].record(s)
+        for j, b in enumerate(Bs):
+            assert gemv(i * len(Bs) + j, b) == 0
+            if evs:
+                evs[3 + j].record(s)
+
+    for i in range(args.warmup):
+        step(i, None)
+    torch.cuda.synchronize()
+    n_ev = 3 + len(Bs)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(args.steps)]
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(s)
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    t_end.record(s)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    per = {n: float(np.mean([evs[i][k].elapsed_time(evs[i][k + 1]) for i in range(args.steps)]))
+           for k, n in enumerate(names)}
+
+    flops = 2.0 * M * N * K
+    quant_bytes = M * K * 2 + M * K / 2 + M * K / 16
+    gemm_tflops = flops / (per["gemm"] * 1e-3) / 1e12
+    prefill_tflops = flops / ((per["quant"] + per["gemm"]) * 1e-3) / 1e12
+    decode = {}
+    for b in Bs:
+        nbytes = N * K * 3 / 8 + N * 8 * 2 + b * K * 2 + b * N * 4
+        gbs = nbytes / (per[f"gemv_b{b}"] * 1e-3) / 1e9
+        decode[f"b{b}"] = {"us": per[f"gemv_b{b}"] * 1e3, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
+                           "bytes": nbytes}
+
+    out = {
+        "metric": METRIC, "value": prefill_tflops, "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": total_ms / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": "8B-scale MLP up-projection: K=4096, N=12288, prefill M=2048 (NVFP4 W4A4), "
+                               "decode B=1,4 (LUT3 per-row fp16 tables)",
+                   "M": M, "N": N, "K": K, "decode_batches": list(Bs), "static_G_x": G_x_host,
+                   "decode_weight_copies": n_w, "x_copies": n_x},
+        "prefill": {"quant_us": per["quant"] * 1e3, "quant_GB/s": quant_bytes / (per["quant"] * 1e-3) / 1e9,
+                    "gemm_us": per["gemm"] * 1e3, "gemm_TFLOP/s": gemm_tflops,
+                    "frac_fp16_mfma_peak": gemm_tflops / PEAK_FP16_TFLOPS,
+                    "frac_fp4_peak": gemm_tflops / PEAK_FP4_TFLOPS,
+                    "linear_TFLOP/s_incl_quant": prefill_tflops},
+        "decode": decode,
+        "pack_ms": {"nvfp4": t_pack_nvfp4, "lut3_per_row": t_pack_lut},
+        "roofline": {"bound": "mfma", "kernel": "nvfp4_gemm_kernel", "achieved": gemm_tflops,
+                     "peak": PEAK_FP16_TFLOPS, "unit": "TFLOP/s", "frac": gemm_tflops / PEAK_FP16_TFLOPS,
+                     "traffic": None,
+                     "note": "exact NVFP4 operands are dequantized to fp16 and multiplied on fp16 MFMA; "
+                             "frac of the dense FP4 peak is prefill.frac_fp4_peak"},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, w, X, np.float32(G_x_host), xds[1])
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -267,8 +267,11 @@ __global__ __launch_bounds__(256) void amax_f32_kernel(const float* __restrict__
   float m = 0.0f;
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
     m = fmaxf(m, fabsf(x[i]));
+  __shared__ float part[4];
   m = wave_max(m);
-  if ((threadIdx.x & 63) == 0) atomic_max_nonneg(out, m);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) atomic_max_nonneg(out, fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3])));
 }
 
 }  // namespace
@@ -304,7 +307,7 @@ hipError_t launch_pack_lut(const float* W, int64_t N, int64_t K, const uint16_t*
   }
   hipLaunchKernelGGL(zero_f32_one, dim3(1), dim3(1), 0, s, out.G);
   int64_t nb = (N * K + 255) / 256;
-  if (nb > 4096) nb = 4096;
+  if (nb > 1024) nb = 1024;
   if (nb < 1) nb = 1;
   hipLaunchKernelGGL(amax_f32_kernel, dim3((unsigned)nb), dim3(256), 0, s, W, N * K, out.G);
   hipLaunchKernelGGL(finalize_g, dim3(1), dim3(1), 0, s, out.G);

@@ -22,6 +22,15 @@ __global__ void finalize_global_scale_kernel(float* p) {
 
 __global__ void copy_float_kernel(const float* src, float* dst) { *dst = *src; }
 
+// Workgroup maximum, then one atomic per workgroup (a few hundred in total).
+__device__ inline void block_max_to(float* out, float m) {
+  __shared__ float part[4];
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) atomic_max_nonneg(out, fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3])));
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void amax_kernel(const T* __restrict__ x, int64_t n_vec,
                                                    int64_t n, float* out);
@@ -45,8 +54,7 @@ __global__ __launch_bounds__(256) void amax_kernel<uint16_t>(const uint16_t* __r
   for (int64_t i = n_vec * 8 + blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
     m = fmaxf(m, fabsf(__uint_as_float((uint32_t)x[i] << 16)));
-  m = wave_max(m);
-  if ((threadIdx.x & 63) == 0) atomic_max_nonneg(out, m);
+  block_max_to(out, m);
 }
 
 // fp32: 4 elements per 16-byte vector
@@ -63,8 +71,7 @@ __global__ __launch_bounds__(256) void amax_kernel<float>(const float* __restric
   for (int64_t i = n_vec * 4 + blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
     m = fmaxf(m, fabsf(x[i]));
-  m = wave_max(m);
-  if ((threadIdx.x & 63) == 0) atomic_max_nonneg(out, m);
+  block_max_to(out, m);
 }
 
 // ------------------------------------------------------------ tile quantizer
@@ -157,7 +164,7 @@ __global__ __launch_bounds__(256) void quantize_tiles_kernel(const T* __restrict
 // ------------------------------------------------------------ launchers
 static int grid_for(int64_t n_vec) {
   int64_t b = (n_vec + 255) / 256;
-  if (b > 4096) b = 4096;
+  if (b > 1024) b = 1024;
   if (b < 1) b = 1;
   return (int)b;
 }
