@@ -12,15 +12,24 @@
 // block scale) and accumulates v_mfma_f32_32x32x16_f16 products in fp32.  The
 // global scales are applied once in the epilogue.
 //
-// Structure: a 256-thread workgroup covers a 256x256 output tile as 2x2
-// wavefronts of 128x128; each wavefront keeps 4x4 32x32 fp32 accumulator
-// blocks.  Operands stream straight from the tiled NVFP4 layout: one 32-row x
-// 64-column tile is 1 KiB of codes, read by one wavefront-wide 16-byte load
-// (lane l: row l%32, columns 32*(l/32) .. +31 of the tile), plus 2 scale bytes
-// per lane.  Within a 64-column step, MFMA sub-step s consumes columns
-// 32*(l/32) + 8s .. +7 on both operands (a permutation of K shared by A and W,
-// which leaves the sum unchanged).  The next step's operands are loaded while
-// the current step's MFMAs run.
+// Structure
+//  * a workgroup of 2 x WN wavefronts covers a 256 x (32*NBW*WN) output tile;
+//    each wavefront owns 128 x 32*NBW (4 x NBW accumulator blocks of 32x32),
+//    two wavefronts per SIMD;
+//  * operands stay compressed (4.5 bits/element) until they reach registers:
+//    a ring of kStages LDS stages, each holding the raw code and scale tiles
+//    of KS 64-column K steps, is filled by direct global->LDS loads
+//    (global_load_lds_dwordx4 / _dword) kStages-1 stages ahead, so the HBM
+//    and L2 latency is hidden without spending VGPRs on prefetch; one
+//    workgroup barrier per stage;
+//  * within a stage, a 32x64 code tile is one contiguous KiB; the loading
+//    lane i fetches 16-byte chunk 2*(i%32) + i/32 so that the consuming lane
+//    l (row l%32, columns 32*(l/32)..+31) reads LDS bytes 16l..16l+15
+//    (conflict-free ds_read_b128);
+//  * MFMA sub-step s of a K step consumes columns 32*(l/32) + 8s .. +7 on both
+//    operands (a permutation of K shared by A and W);
+//  * workgroups are numbered so that the 8 XCDs each own a contiguous range
+//    of output-column panels (W panels stay in one XCD's L2).
 #include "dq_device.hpp"
 #include "dq_internal.hpp"
 
@@ -28,34 +37,31 @@ namespace dq {
 
 namespace {
 
-constexpr int kWaveM = 128;
-constexpr int kWaveN = 128;
 constexpr int kBlkM = 256;
-constexpr int kBlkN = 256;
+constexpr int kLdsBudget = 150 * 1024;   // of gfx950's 160 KiB
 
-struct Operand {
-  uint4_t code[4];
-  uint32_t scale[4];
+// Workgroup geometry: WN wavefront columns x 2 wavefront rows; a wavefront
+// owns 128 rows x 32*NBW columns, so the workgroup tile is 256 x 32*NBW*WN.
+template <int WN, int NBW, int KS>
+struct Geo {
+  static constexpr int waves = 2 * WN;
+  static constexpr int threads = 64 * waves;
+  static constexpr int bn = 32 * NBW * WN;     // workgroup tile columns
+  static constexpr int wt = bn / 32;           // W code tiles per K step
+  static constexpr int ks = KS;                // 64-column K steps per stage (one barrier each)
+  // LDS byte layout of one stage, per K step u: A codes (8 KiB), W codes,
+  // A scales (1 KiB), W scales
+  static constexpr int step_bytes = 8 * 1024 + wt * 1024 + 8 * 128 + wt * 128;
+  static constexpr int a_codes = 0;
+  static constexpr int w_codes = 8 * 1024;
+  static constexpr int a_scales = w_codes + wt * 1024;
+  static constexpr int w_scales = a_scales + 8 * 128;
+  static constexpr int bytes = KS * step_bytes;
+  static constexpr int stages = kLdsBudget / bytes;   // ring depth
+  // direct-to-LDS instructions per K step: 8 + wt code tiles, (8 + wt) / 2 scale pairs
+  static constexpr int code_loads = 8 + wt;
+  static constexpr int scale_loads = (8 + wt) / 2;
 };
-
-__device__ inline void load_operand(const uint8_t* __restrict__ codes, const uint8_t* __restrict__ scales,
-                                    int64_t tile_row0, int64_t n_tile_rows, int64_t kt, int64_t KT,
-                                    int lane, Operand& op) {
-  const int lane_code = (lane & 31) * 32 + (lane >> 5) * 16;
-  const int lane_scale = (lane & 31) * 4 + (lane >> 5) * 2;
-#pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    const int64_t tr = tile_row0 + b;
-    if (tr < n_tile_rows) {
-      const int64_t tile = tr * KT + kt;
-      op.code[b] = *reinterpret_cast<const uint4_t*>(codes + tile * 1024 + lane_code);
-      op.scale[b] = *reinterpret_cast<const uint16_t*>(scales + tile * 128 + lane_scale);
-    } else {
-      op.code[b] = uint4_t{0u, 0u, 0u, 0u};
-      op.scale[b] = 0u;
-    }
-  }
-}
 
 // 8 E2M1 codes (one dword) times an fp16 block scale -> 8 exact fp16 values.
 __device__ inline half8_t dequant8(uint32_t w, half2_t s) {
@@ -73,57 +79,180 @@ __device__ inline void scale_pairs(uint32_t sc, half2_t& lo, half2_t& hi) {
   hi = half2_t{s[1], s[1]};
 }
 
-template <int OUT>
-__global__ __launch_bounds__(256, 1) void nvfp4_gemm_kernel(
+// Number of direct-to-LDS load instructions wavefront `wave` issues per stage
+// (code tiles round-robin over the wavefronts, then scale instructions).
+template <class Gm>
+__host__ __device__ constexpr int loads_per_stage(int wave) {
+  return Gm::ks * ((Gm::code_loads - wave + Gm::waves - 1) / Gm::waves +
+                   (Gm::scale_loads - wave + Gm::waves - 1) / Gm::waves);
+}
+
+// Issue the direct-to-LDS loads of one K step into `stage`.  Code tiles are
+// distributed round-robin over the wavefronts; scale tiles are 128 bytes and
+// one dword instruction covers two of them (lanes 0..31, 32..63).  Tiles past
+// the end of an operand read a clamped, in-bounds address so that every
+// wavefront issues a fixed number of loads (the data is zeroed on use).
+template <class Gm>
+__device__ inline void issue_stage(uint8_t* stage, const uint8_t* __restrict__ a_codes,
+                                   const uint8_t* __restrict__ a_scales, const uint8_t* __restrict__ w_codes,
+                                   const uint8_t* __restrict__ w_scales, int64_t a_tr0, int64_t a_tiles_r,
+                                   int64_t w_tr0, int64_t w_tiles_r, int64_t kt, int64_t KT, int wave, int lane) {
+  const int chunk = 2 * (lane & 31) + (lane >> 5);      // global 16-byte chunk fetched by this lane
+  for (int u = 0; u < Gm::ks; ++u, ++kt, stage += Gm::step_bytes) {
+  const int64_t ktc = kt < KT ? kt : KT - 1;             // past the end of K: reload the last step
+  for (int t = wave; t < Gm::code_loads; t += Gm::waves) {
+    const bool is_a = t < 8;
+    const int b = is_a ? t : t - 8;
+    const int64_t lim = is_a ? a_tiles_r : w_tiles_r;
+    int64_t tr = (is_a ? a_tr0 : w_tr0) + b;
+    tr = tr < lim ? tr : lim - 1;
+    const uint8_t* src = (is_a ? a_codes : w_codes) + (tr * KT + ktc) * 1024 + chunk * 16;
+    uint8_t* dst = stage + (is_a ? Gm::a_codes : Gm::w_codes) + b * 1024;
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src), reinterpret_cast<void*>(dst), 16, 0, 0);
+  }
+  for (int t = wave; t < Gm::scale_loads; t += Gm::waves) {
+    const bool is_a = t < 4;
+    const int b = 2 * (is_a ? t : t - 4) + (lane >> 5);
+    const int64_t lim = is_a ? a_tiles_r : w_tiles_r;
+    int64_t tr = (is_a ? a_tr0 : w_tr0) + b;
+    tr = tr < lim ? tr : lim - 1;
+    const uint8_t* src = (is_a ? a_scales : w_scales) + (tr * KT + ktc) * 128 + (lane & 31) * 4;
+    uint8_t* dst = stage + (is_a ? Gm::a_scales : Gm::w_scales) + (b & ~1) * 128;
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src), reinterpret_cast<void*>(dst), 4, 0, 0);
+  }
+  }
+}
+
+// s_waitcnt vmcnt(n) (n < 64) with expcnt / lgkmcnt left at their maximum.
+// gfx9 encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at [15:14].
+template <int n>
+__device__ inline void wait_vm() {
+  __builtin_amdgcn_s_waitcnt((n & 0xF) | (0x7 << 4) | (0xF << 8) | ((n >> 4) << 14));
+}
+__device__ inline void wait_vm_dyn(int n) {
+  switch (n) {
+#define DQ_VM(k) case k: wait_vm<k>(); break;
+    DQ_VM(0) DQ_VM(1) DQ_VM(2) DQ_VM(3) DQ_VM(4) DQ_VM(5) DQ_VM(6) DQ_VM(7) DQ_VM(8) DQ_VM(9)
+    DQ_VM(10) DQ_VM(11) DQ_VM(12) DQ_VM(13) DQ_VM(14) DQ_VM(15) DQ_VM(16) DQ_VM(17) DQ_VM(18)
+    DQ_VM(19) DQ_VM(20) DQ_VM(21) DQ_VM(22) DQ_VM(23) DQ_VM(24) DQ_VM(25) DQ_VM(26) DQ_VM(27)
+    DQ_VM(28) DQ_VM(29) DQ_VM(30) DQ_VM(31)
+#undef DQ_VM
+    default: wait_vm<0>(); break;
+  }
+}
+
+// Workgroup barrier without the release/acquire fences of __syncthreads (which
+// would also wait for every outstanding prefetch); the empty asm statements
+// keep the compiler from moving LDS accesses across it.
+__device__ inline void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int WN, int NBW, int KS, int OUT>
+__global__ __launch_bounds__(64 * 2 * WN, 1) void nvfp4_gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales, const float* __restrict__ Ga,
     const uint8_t* __restrict__ w_codes, const uint8_t* __restrict__ w_scales, const float* __restrict__ Gw,
-    int64_t M, int64_t N, int64_t a_tile_rows, int64_t w_tile_rows, int64_t KT, void* __restrict__ Y,
-    int64_t tiles_n) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int64_t bm = blockIdx.x / tiles_n, bn = blockIdx.x % tiles_n;
-  const int64_t m0 = bm * kBlkM + (wave & 1) * kWaveM;
-  const int64_t n0 = bn * kBlkN + (wave >> 1) * kWaveN;
-  const int64_t a_tr0 = m0 / 32, w_tr0 = n0 / 32;
+    int64_t M, int64_t N, int64_t a_tiles_r, int64_t w_tiles_r, int64_t KT, void* __restrict__ Y,
+    int64_t tiles_m, int64_t tiles_n) {
+  typedef Geo<WN, NBW, KS> Gm;
+  constexpr int kStages = Gm::stages;
+  extern __shared__ __align__(16) uint8_t smem[];
 
-  float16_t acc[4][4];
+  const int lane = threadIdx.x & 63;
+  // wavefront index as a uniform (scalar) value: the LDS destination of the
+  // direct loads lives in M0 and must not look divergent to the compiler
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // XCD-aware numbering: workgroup b runs on XCD b % 8; give each XCD a
+  // contiguous range of tiles, ordered column-panel-major.
+  const int64_t nb = tiles_m * tiles_n;
+  int64_t logical = blockIdx.x;
+  if (nb % 8 == 0) logical = (int64_t)(blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8;
+  const int64_t bm = logical % tiles_m, bn = logical / tiles_m;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int64_t a_tr0 = bm * (kBlkM / 32), w_tr0 = bn * Gm::wt;
+  const int64_t m0 = bm * kBlkM + wm * 128;
+  const int64_t n0 = bn * Gm::bn + wn * 32 * NBW;
+
+  float16_t acc[4][NBW];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = float16_t{};
+    for (int j = 0; j < NBW; ++j) acc[i][j] = float16_t{};
 
-  Operand a_cur, w_cur, a_nxt, w_nxt;
-  load_operand(a_codes, a_scales, a_tr0, a_tile_rows, 0, KT, lane, a_cur);
-  load_operand(w_codes, w_scales, w_tr0, w_tile_rows, 0, KT, lane, w_cur);
+  const int64_t NST = (KT + KS - 1) / KS;     // stages of KS K steps
+  // prologue: stages 0 .. kStages-2
+#pragma unroll
+  for (int st = 0; st < kStages - 1; ++st)
+    if (st < NST)
+      issue_stage<Gm>(smem + st * Gm::bytes, a_codes, a_scales, w_codes, w_scales, a_tr0, a_tiles_r, w_tr0,
+                      w_tiles_r, (int64_t)st * KS, KT, wave, lane);
+  const int L = loads_per_stage<Gm>(wave);
 
-  for (int64_t kt = 0; kt < KT; ++kt) {
-    if (kt + 1 < KT) {
-      load_operand(a_codes, a_scales, a_tr0, a_tile_rows, kt + 1, KT, lane, a_nxt);
-      load_operand(w_codes, w_scales, w_tr0, w_tile_rows, kt + 1, KT, lane, w_nxt);
-    }
-    half2_t a_s[4][2], w_s[4][2];
+  // rows / columns of this wavefront that exist (zero inputs elsewhere)
+  bool a_ok[4], w_ok[NBW];
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      scale_pairs(a_cur.scale[b], a_s[b][0], a_s[b][1]);
-      scale_pairs(w_cur.scale[b], w_s[b][0], w_s[b][1]);
-    }
+  for (int i = 0; i < 4; ++i) a_ok[i] = (m0 / 32 + i) < a_tiles_r;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      half8_t af[4], wf[4];
+  for (int j = 0; j < NBW; ++j) w_ok[j] = (n0 / 32 + j) < w_tiles_r;
+  const int lane_scale = (lane & 31) * 4 + (lane >> 5) * 2;
+
+  for (int64_t st = 0; st < NST; ++st) {
+    // wait until this wavefront's loads of stage st have landed (the loads of
+    // the stages issued after it may stay in flight), then for all wavefronts
+    const int ahead = (int)min((int64_t)kStages - 2, NST - 1 - st);
+    wait_vm_dyn(ahead * L);
+    lds_barrier();
+    // refill the stage consumed in the previous iteration
+    if (st + kStages - 1 < NST)
+      issue_stage<Gm>(smem + ((st + kStages - 1) % kStages) * Gm::bytes, a_codes, a_scales, w_codes, w_scales,
+                      a_tr0, a_tiles_r, w_tr0, w_tiles_r, (st + kStages - 1) * KS, KT, wave, lane);
+
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        af[b] = dequant8(a_cur.code[b][s], a_s[b][s >> 1]);
-        wf[b] = dequant8(w_cur.code[b][s], w_s[b][s >> 1]);
+    for (int u = 0; u < KS; ++u) {
+      if (st * KS + u >= KT) break;                    // a partial last stage
+      const uint8_t* stg = smem + (st % kStages) * Gm::bytes + u * Gm::step_bytes;
+      uint4_t ac[4], wc[NBW];
+      uint32_t asc[4], wsc[NBW];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int b = wm * 4 + i;
+        ac[i] = *reinterpret_cast<const uint4_t*>(stg + Gm::a_codes + b * 1024 + lane * 16);
+        asc[i] = *reinterpret_cast<const uint16_t*>(stg + Gm::a_scales + b * 128 + lane_scale);
+        if (!a_ok[i]) {
+          ac[i] = uint4_t{0u, 0u, 0u, 0u};
+          asc[i] = 0u;
+        }
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < NBW; ++j) {
+        const int b = wn * NBW + j;
+        wc[j] = *reinterpret_cast<const uint4_t*>(stg + Gm::w_codes + b * 1024 + lane * 16);
+        wsc[j] = *reinterpret_cast<const uint16_t*>(stg + Gm::w_scales + b * 128 + lane_scale);
+        if (!w_ok[j]) {
+          wc[j] = uint4_t{0u, 0u, 0u, 0u};
+          wsc[j] = 0u;
+        }
+      }
+      half2_t as_[4][2], ws_[NBW][2];
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], wf[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < KT) {
-      a_cur = a_nxt;
-      w_cur = w_nxt;
+      for (int i = 0; i < 4; ++i) scale_pairs(asc[i], as_[i][0], as_[i][1]);
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) scale_pairs(wsc[j], ws_[j][0], ws_[j][1]);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        half8_t af[4], wf[NBW];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) af[i] = dequant8(ac[i][s], as_[i][s >> 1]);
+#pragma unroll
+        for (int j = 0; j < NBW; ++j) wf[j] = dequant8(wc[j][s], ws_[j][s >> 1]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < NBW; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], wf[j], acc[i][j], 0, 0, 0);
+      }
     }
   }
 
@@ -133,7 +262,7 @@ __global__ __launch_bounds__(256, 1) void nvfp4_gemm_kernel(
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < NBW; ++j) {
       const int64_t col = n0 + j * 32 + col_in;
       if (col >= N) continue;
 #pragma unroll
@@ -151,22 +280,30 @@ __global__ __launch_bounds__(256, 1) void nvfp4_gemm_kernel(
   }
 }
 
+template <int WN, int NBW, int KS>
+hipError_t launch_geo(const GemmArgs& a, hipStream_t s) {
+  typedef Geo<WN, NBW, KS> Gm;
+  const int64_t a_tiles_r = round_up(a.M, 32) / 32;
+  const int64_t w_tiles_r = round_up(a.N, 32) / 32;
+  const int64_t KT = round_up(a.K, 64) / 64;
+  const int64_t tiles_m = (a.M + kBlkM - 1) / kBlkM, tiles_n = (a.N + Gm::bn - 1) / Gm::bn;
+  const size_t lds = (size_t)Gm::stages * Gm::bytes;
+  auto kern = a.out_kind == 0 ? nvfp4_gemm_kernel<WN, NBW, KS, 0> : nvfp4_gemm_kernel<WN, NBW, KS, 1>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_m * tiles_n)), dim3(Gm::threads), lds, s, a.A.codes, a.A.scales,
+                     a.A.G, a.W.codes, a.W.scales, a.W.G, a.M, a.N, a_tiles_r, w_tiles_r, KT, a.Y, tiles_m, tiles_n);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
   if (a.M == 0 || a.N == 0) return hipSuccess;
-  const int64_t a_tile_rows = round_up(a.M, 32) / 32;
-  const int64_t w_tile_rows = round_up(a.N, 32) / 32;
-  const int64_t KT = round_up(a.K, 64) / 64;
-  const int64_t tiles_m = (a.M + kBlkM - 1) / kBlkM, tiles_n = (a.N + kBlkN - 1) / kBlkN;
-  const dim3 grid((unsigned)(tiles_m * tiles_n));
-  if (a.out_kind == 0)
-    hipLaunchKernelGGL(nvfp4_gemm_kernel<0>, grid, dim3(256), 0, s, a.A.codes, a.A.scales, a.A.G,
-                       a.W.codes, a.W.scales, a.W.G, a.M, a.N, a_tile_rows, w_tile_rows, KT, a.Y, tiles_n);
-  else
-    hipLaunchKernelGGL(nvfp4_gemm_kernel<1>, grid, dim3(256), 0, s, a.A.codes, a.A.scales, a.A.G,
-                       a.W.codes, a.W.scales, a.W.G, a.M, a.N, a_tile_rows, w_tile_rows, KT, a.Y, tiles_n);
-  return hipGetLastError();
+  // 256x256 workgroup tiles as 2x4 wavefronts of 128x64 (two wavefronts per
+  // SIMD hide each other's LDS / barrier / load stalls).
+  return launch_geo<4, 2, 2>(a, s);
 }
 
 }  // namespace dq
