@@ -8,21 +8,21 @@
 // Design (MI355X: 8 TB/s HBM against ~39 T VALU lane-ops/s leaves under two
 // VALU instructions per 3-bit weight):
 //  * codes stream with one coalesced wavefront load per 16-row x 128-column
-//    tile (64 lanes x 12 bytes for 3 bits, x 8 bytes for 2 bits); every
-//    wavefront issues all of its code loads (up to a ring of 8 tiles) before
-//    touching LDS, so the whole matrix is in flight early;
+//    chunk of a row tile (64 lanes x 12 bytes for 3 bits, x 8 bytes for 2
+//    bits), a ring of loads kept in flight ahead of use;
 //  * each 32-code group is split into eight 4-code byte selectors with shifts
 //    and masks (the bit layout in dq.h is chosen for this), and v_perm_b32
 //    looks the 4 codes up in register-resident byte tables (low bytes and
 //    high bytes of the row's fp16 entries), then interleaves them into fp16
-//    pairs: about 1.5 VALU instructions per 3-bit weight;
+//    pairs: about 1.6 VALU instructions per 3-bit weight;
 //  * the multiply-accumulate runs on MFMA (v_mfma_f32_16x16x32_f16: 16 weight
 //    rows x 32 k x 16 batch columns), so batch 1..16 costs the same VALU work;
-//  * activations are staged once per workgroup and K-piece into LDS as fp16,
-//    rescaled by a power of two per batch row (exact products with the fp16
-//    table); the wavefronts of a workgroup split K and reduce through LDS in a
-//    fixed order, so results are deterministic.
+//  * activations are staged once per workgroup into LDS as fp16, rescaled by
+//    a power of two per batch row (exact products with the fp16 table); the
+//    wavefronts of a workgroup split K and reduce through LDS in a fixed
+//    order, so results are deterministic.
 #include <algorithm>
+#include <cstdint>
 
 #include "dq_device.hpp"
 #include "dq_internal.hpp"
@@ -31,8 +31,7 @@ namespace dq {
 
 namespace {
 
-constexpr int kRing = 8;        // code loads in flight per wavefront
-constexpr int kStageVec = 4;    // 8-element activation vectors staged per thread and piece
+constexpr int kStageVec = 4;    // register-staged 8-element activation vectors per thread and piece
 
 // One lane's 32-code group: 12 bytes (3 bits) or 8 bytes (2 bits).  Plain
 // structs, so that sizeof is exactly the group size (a 3-element vector type
@@ -107,190 +106,213 @@ __device__ inline half8_t scale_half8(half8_t v, half2_t s) {
   return half8_t{a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
 }
 
-// Tables of one row (PER_ROW) or of the grid (PAPER_GRID): low bytes and high
-// bytes of the 2^BITS fp16 entries, as v_perm_b32 pools.
+// Table of one row (PER_ROW) or the grid (PAPER_GRID): the 2^BITS fp16
+// entries as raw dwords (2 bits: the upper half is unused).
 template <int BITS>
-__device__ inline void load_tables(const uint16_t* L, uint32_t& tl0, uint32_t& tl1, uint32_t& th0, uint32_t& th1) {
+__device__ inline uint4_t load_table(const uint16_t* L) {
+  if (BITS == 3) return *reinterpret_cast<const uint4_t*>(L);
+  const uint2_t d = *reinterpret_cast<const uint2_t*>(L);
+  return uint4_t{d[0], d[1], 0u, 0u};
+}
+
+// Low bytes and high bytes of the table entries, as v_perm_b32 pools.
+template <int BITS>
+__device__ inline void table_pools(const uint4_t& d, uint32_t& tl0, uint32_t& tl1, uint32_t& th0, uint32_t& th1) {
+  tl0 = __builtin_amdgcn_perm(d[1], d[0], 0x06040200u);
+  th0 = __builtin_amdgcn_perm(d[1], d[0], 0x07050301u);
   if (BITS == 3) {
-    const uint4_t d = *reinterpret_cast<const uint4_t*>(L);
-    tl0 = __builtin_amdgcn_perm(d[1], d[0], 0x06040200u);
-    th0 = __builtin_amdgcn_perm(d[1], d[0], 0x07050301u);
     tl1 = __builtin_amdgcn_perm(d[3], d[2], 0x06040200u);
     th1 = __builtin_amdgcn_perm(d[3], d[2], 0x07050301u);
   } else {
-    const uint2_t d = *reinterpret_cast<const uint2_t*>(L);
-    tl0 = tl1 = __builtin_amdgcn_perm(d[1], d[0], 0x06040200u);
-    th0 = th1 = __builtin_amdgcn_perm(d[1], d[0], 0x07050301u);
+    tl1 = tl0;
+    th1 = th0;
   }
 }
 
 // Work decomposition.  A workgroup holds RT row tiles x KS K-splits
-// (W = RT*KS <= 8 wavefronts).  K is processed in pieces of PK 128-column chunks;
-// for each piece the workgroup stages the activations once (fp16, rescaled by
-// a power of two so that the piece maximum of each batch row lands in
-// [2^14, 2^15)), then wavefront (rt, ks) consumes chunks ks, ks+KS, ... of the
-// piece for row tile rt.  Each wavefront walks a fixed sequence of CPW8 slots
-// per piece (a multiple of 8) and keeps the code loads of the next 8 slots in
-// flight across piece boundaries.  The KS partial sums of a row tile are
-// reduced through LDS in a fixed order (deterministic).
+// (W = RT*KS wavefronts); wavefront (rt, ks) consumes chunks ks, ks+KS, ...
+// of row tile rt.  Each wavefront walks a fixed sequence of CPW slots per
+// activation piece (a multiple of its load ring) and keeps RING code loads in
+// flight.  A slot past the end of the piece's chunks re-reads the piece's last
+// chunk and multiplies it by a zero activation chunk instead of branching, so
+// the slot loop has no data-dependent control flow and the compiler can
+// interleave the lookups of one slot with the MFMAs of the previous one.  The
+// KS partial sums of a row tile are reduced through LDS in a fixed order.
+//
+// Two kernels:
+//  * single piece (all of K staged at once; B*K up to ~75 K elements): the
+//    raw activations go straight from global memory into LDS (one wavefront
+//    load per 128-element chunk, no registers held), then are converted in
+//    place; few registers, so several small workgroups share a compute unit;
+//  * several pieces (larger B*K): each piece is staged through registers, and
+//    the next piece's activations are loaded while the current one is
+//    consumed.
+//
+// Memory order.  The weight codes stream from HBM as long row-hit bursts that
+// keep every channel busy; a scattered miss issued behind them (the
+// activations, shared by all workgroups) waits until the streams drain.  So a
+// workgroup stages its first activation piece before it issues any code load,
+// and with several pieces the workgroups of each XCD first pull the whole
+// activation matrix into that XCD's L2, which the later pieces then hit.
 struct GemvPlan {
-  int RT, KS, PK, CPW8, npieces;
+  int RT, KS, PK, CPW, npieces;
   int64_t tiles, KC;
 };
 
-template <int BITS, int MODE>
-__global__ __launch_bounds__(512) void lut_gemv_kernel(const uint16_t* __restrict__ x, int B, int64_t K,
-                                                       const uint8_t* __restrict__ codes,
-                                                       const uint16_t* __restrict__ lut,
-                                                       const uint8_t* __restrict__ scales,
-                                                       const float* __restrict__ Gp, int64_t N, GemvPlan plan,
-                                                       int out_kind, void* __restrict__ y) {
+// Raw buffer loads (LLVM AMDGPU intrinsics): a scalar resource (base, size),
+// a per-lane VGPR offset and a uniform SGPR offset, so the address of a code
+// load costs no VALU instruction; offsets past the resource size read zero.
+typedef int32_t i32x2_t __attribute__((ext_vector_type(2)));
+typedef int32_t i32x3_t __attribute__((ext_vector_type(3)));
+typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
+__device__ i32x2_t raw_buffer_load_b64(i32x4_t rsrc, int32_t voff, int32_t soff,
+                                       int32_t aux) __asm("llvm.amdgcn.raw.buffer.load.v2i32");
+__device__ i32x3_t raw_buffer_load_b96(i32x4_t rsrc, int32_t voff, int32_t soff,
+                                       int32_t aux) __asm("llvm.amdgcn.raw.buffer.load.v3i32");
+__device__ int16_t raw_buffer_load_b16(i32x4_t rsrc, int32_t voff, int32_t soff,
+                                       int32_t aux) __asm("llvm.amdgcn.raw.buffer.load.i16");
+
+// gfx9 buffer resource over [p, p + bytes): 48-bit base, stride 0, byte range,
+// 32-bit data format (raw loads ignore the format)
+__device__ inline i32x4_t buffer_resource(const void* p, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  return i32x4_t{(int32_t)(uint32_t)a, (int32_t)(uint32_t)((a >> 32) & 0xFFFFu), (int32_t)bytes, 0x00020000};
+}
+
+// One wavefront's code stream over its row tile: a ring of RING chunk loads
+// (and, for PAPER_GRID, of the chunk's two block-scale bytes).
+template <int BITS, int MODE, int RING>
+struct CodeStream {
   typedef typename CodeVec<BITS>::type cvec;
-  constexpr int GB = CodeVec<BITS>::bytes;
-  extern __shared__ __align__(16) uint8_t smem[];
-  __shared__ uint32_t piece_max[16];
+  static constexpr int kChunkBytes = 64 * CodeVec<BITS>::bytes;
+  i32x4_t rcodes;         // the tile's codes
+  i32x4_t rscales;        // PAPER_GRID: the tile's block scales
+  int32_t lane_code;      // this lane's group within a chunk: lane * group bytes
+  int32_t lane_scale;     // this lane's scale pair within a chunk: lane * 2
+  int PK, KS, ks, KC;
+  cvec ring[RING];
+  uint32_t sring[RING];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int nthreads = blockDim.x;
-  const int rt = wave / plan.KS, ks = wave % plan.KS;
-  const int64_t tile = (int64_t)blockIdx.x * plan.RT + rt;
-  const bool tile_ok = tile < plan.tiles;
-  const int64_t KC = plan.KC;
-  const int PK = plan.PK, CPW8 = plan.CPW8, KS = plan.KS;
+  __device__ void init(const uint8_t* tile_codes, const uint8_t* tile_scales, int lane, int PK_, int KS_, int ks_,
+                       int KC_) {
+    rcodes = buffer_resource(tile_codes, (uint32_t)KC_ * kChunkBytes);
+    if (MODE == 1) rscales = buffer_resource(tile_scales, (uint32_t)KC_ * 128);
+    lane_code = lane * CodeVec<BITS>::bytes;
+    lane_scale = lane * 2;
+    PK = PK_;
+    KS = KS_;
+    ks = ks_;
+    KC = KC_;
+  }
+  // chunk of slot s in piece p, clamped to the piece's last chunk (in bounds)
+  __device__ int chunk(int p, int s) const { return min(p * PK + s * KS + ks, min((p + 1) * PK, KC) - 1); }
+  __device__ void load(int r, int c) {
+    if constexpr (BITS == 3) {
+      const i32x3_t v = raw_buffer_load_b96(rcodes, lane_code, c * kChunkBytes, 0);
+      ring[r] = cvec{{(uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2]}};
+    } else {
+      const i32x2_t v = raw_buffer_load_b64(rcodes, lane_code, c * kChunkBytes, 0);
+      ring[r] = cvec{{(uint32_t)v[0], (uint32_t)v[1]}};
+    }
+    if (MODE == 1) sring[r] = (uint16_t)raw_buffer_load_b16(rscales, lane_scale, c * 128, 0);
+  }
+};
 
-  // slot s of piece p -> chunk p*PK + s*KS + ks (valid when inside the piece and tile_ok)
-  auto slot_chunk = [&](int p, int s, int64_t& c) -> bool {
-    const int64_t local = (int64_t)s * KS + ks;
-    const int64_t len = min((int64_t)PK, KC - (int64_t)p * PK);
-    c = (int64_t)p * PK + local;
-    return tile_ok && local < len;
+// Consume the CPW slots of piece p (activation chunks of the staged piece
+// start at xrow; chunk PK of every staged row is zero), prefetching RING slots
+// ahead, into piece pn once the sequence wraps.  pacc[st] accumulates the
+// st-th 32-column step of every chunk, so consecutive MFMAs are independent.
+template <int BITS, int MODE, int RING>
+__device__ __forceinline__ void consume(CodeStream<BITS, MODE, RING>& cs, int p, int pn, int CPW,
+                                        const _Float16* xrow, int zero_shift, const uint4_t& tab,
+                                        float4_t (&pacc)[4]) {
+  uint32_t tl0, tl1, th0, th1;
+  table_pools<BITS>(tab, tl0, tl1, th0, th1);
+  // activation fragments of slot s (4 x 8 fp16 per lane); those of slot s+1
+  // are read from LDS while slot s computes
+  auto xfrag = [&](int s, half8_t (&f)[4]) {
+    const half8_t* xp = reinterpret_cast<const half8_t*>(xrow + min(s * cs.KS + cs.ks + zero_shift, cs.PK) * 128);
+#pragma unroll
+    for (int st = 0; st < 4; ++st) f[st] = xp[st];
   };
-  const uint8_t* tile_codes = codes + (tile * KC * 64 + lane) * GB;
-
-  // ---- 1. code loads of the first 8 slots
-  cvec ring[kRing];
+  half8_t bf[4];
+  xfrag(0, bf);
+  for (int s0 = 0; s0 < CPW; s0 += RING) {
 #pragma unroll
-  for (int r = 0; r < kRing; ++r) {
-    int64_t c;
-    if (slot_chunk(0, r, c)) ring[r] = *reinterpret_cast<const cvec*>(tile_codes + c * 64 * GB);
-  }
-
-  // ---- 2. lookup tables (lane: row i = lane % 16 of the tile)
-  const int i = lane & 15, q = lane >> 4, j = lane & 15;
-  uint32_t tl0 = 0, tl1 = 0, th0 = 0, th1 = 0;
-  if (tile_ok) load_tables<BITS>(MODE == 0 ? lut + (tile * 16 + i) * (1 << BITS) : lut, tl0, tl1, th0, th1);
-  const uint16_t* sbase = nullptr;
-  if (MODE == 1) sbase = reinterpret_cast<const uint16_t*>(scales + tile * KC * 128) + lane;
-
-  const bool xlane = j < B;
-  const int rowstride = PK * 128 + 8;              // fp16 elements per staged batch row
-  _Float16* xs = reinterpret_cast<_Float16*>(smem);
-  float4_t acc = {0.f, 0.f, 0.f, 0.f};
-
-  for (int p = 0; p < plan.npieces; ++p) {
-    // ---- 3. stage the activation piece (all wavefronts), one pass through registers
-    const int64_t k0 = (int64_t)p * PK * 128;
-    const int len = (int)min((int64_t)PK, KC - (int64_t)p * PK);
-    const int vec_per_row = len * 16;              // 8-element vectors per batch row
-    const int nvec = B * vec_per_row;
-    if ((int)threadIdx.x < B) piece_max[threadIdx.x] = 0u;
-    __syncthreads();
-    uint4_t v[kStageVec];
-#pragma unroll
-    for (int n = 0; n < kStageVec; ++n) {
-      const int f = n * nthreads + threadIdx.x;
-      v[n] = uint4_t{0u, 0u, 0u, 0u};
-      if (f < nvec) {
-        const int jj = f / vec_per_row;
-        const int64_t k = k0 + (int64_t)(f % vec_per_row) * 8;
-        if (k < K) v[n] = *reinterpret_cast<const uint4_t*>(x + (int64_t)jj * K + k);
-        float m = 0.0f;
-#pragma unroll
-        for (int w4 = 0; w4 < 4; ++w4) m = fmaxf(m, fmaxf(fabsf(bf16_lo(v[n][w4])), fabsf(bf16_hi(v[n][w4]))));
-        if (m > 0.0f) atomicMax(&piece_max[jj], __float_as_uint(m));
+    for (int r = 0; r < RING; ++r) {
+      const int s = s0 + r;
+      half8_t bn[4];
+      xfrag(s + 1, bn);   // past CPW: a zero or in-range chunk, never used
+      // keep these reads at the top of the slot (the scheduler would sink
+      // them next to their MFMAs and expose the LDS latency)
+      __builtin_amdgcn_sched_barrier(0);
+      const uint32_t sv = cs.sring[r];
+      uint32_t sel[8];
+      selectors<BITS>(cs.ring[r], sel);
+      // refill the ring slot once its codes are in the selectors
+      const bool wrap = s + RING >= CPW;
+      cs.load(r, wrap ? cs.chunk(pn, s + RING - CPW) : cs.chunk(p, s + RING));
+      half2_t s_lo, s_hi;
+      if (MODE == 1) {
+        const half2_t sc2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sv, 1.0f, false);
+        s_lo = half2_t{sc2[0], sc2[0]};
+        s_hi = half2_t{sc2[1], sc2[1]};
       }
-    }
-    __syncthreads();
 #pragma unroll
-    for (int n = 0; n < kStageVec; ++n) {
-      const int f = n * nthreads + threadIdx.x;
-      if (f < nvec) {
-        const int jj = f / vec_per_row;
-        const uint32_t mb = piece_max[jj];
-        const int e = mb ? min(126, 14 - ((int)((mb >> 23) & 0xFF) - 127)) : 0;
-        const float sc = __builtin_ldexpf(1.0f, e);
-        half8_t h;
-#pragma unroll
-        for (int w4 = 0; w4 < 4; ++w4) {
-          h[2 * w4] = (_Float16)(bf16_lo(v[n][w4]) * sc);
-          h[2 * w4 + 1] = (_Float16)(bf16_hi(v[n][w4]) * sc);
-        }
-        *reinterpret_cast<half8_t*>(xs + jj * rowstride + (f % vec_per_row) * 8) = h;
+      for (int st = 0; st < 4; ++st) {
+        uint32_t a0, a1, a2, a3;
+        lookup4(sel[2 * st], tl0, tl1, th0, th1, a0, a1);
+        lookup4(sel[2 * st + 1], tl0, tl1, th0, th1, a2, a3);
+        half8_t af = as_half8(a0, a1, a2, a3);
+        if (MODE == 1) af = scale_half8(af, st < 2 ? s_lo : s_hi);
+        pacc[st] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf[st], pacc[st], 0, 0, 0);
       }
+#pragma unroll
+      for (int st = 0; st < 4; ++st) bf[st] = bn[st];
     }
+  }
+}
+
+// fp16 rescale exponent of a batch row whose maximum magnitude has bits mb:
+// the maximum lands in [2^14, 2^15)
+__device__ inline int stage_exponent(uint32_t mb) {
+  return mb ? min(126, 14 - ((int)((mb >> 23) & 0xFF) - 127)) : 0;
+}
+
+__device__ inline half8_t to_half8_scaled(const uint4_t& raw, float sc) {
+  half8_t h;
+#pragma unroll
+  for (int w4 = 0; w4 < 4; ++w4) {
+    h[2 * w4] = (_Float16)(bf16_lo(raw[w4]) * sc);
+    h[2 * w4 + 1] = (_Float16)(bf16_hi(raw[w4]) * sc);
+  }
+  return h;
+}
+
+__device__ inline float max_abs8(const uint4_t& raw) {
+  float m = 0.0f;
+#pragma unroll
+  for (int w4 = 0; w4 < 4; ++w4) m = fmaxf(m, fmaxf(fabsf(bf16_lo(raw[w4])), fabsf(bf16_hi(raw[w4]))));
+  return m;
+}
+
+// maximum over the 16-lane group (all 64 lanes must be active)
+__device__ inline float group16_max(float m) {
+  m = fmaxf(m, __shfl_xor(m, 1, 64));
+  m = fmaxf(m, __shfl_xor(m, 2, 64));
+  m = fmaxf(m, __shfl_xor(m, 4, 64));
+  m = fmaxf(m, __shfl_xor(m, 8, 64));
+  return m;
+}
+
+// Reduce the KS partial sums of each row tile in a fixed order and store
+// (lane: batch column j = lane % 16, rows 4q..4q+3 of the tile).
+__device__ inline void reduce_store(float4_t acc, float4_t* red, int wave, int lane, int ks, int KS, bool tile_ok,
+                                    int64_t tile, int64_t N, int out_kind, void* __restrict__ y, bool xlane) {
+  if (KS > 1) {
+    red[wave * 64 + lane] = acc;
     __syncthreads();
-    float unscale = 1.0f;
-    if (xlane && piece_max[j]) unscale = __builtin_ldexpf(1.0f, -min(126, 14 - ((int)((piece_max[j] >> 23) & 0xFF) - 127)));
-
-    // ---- 4. this wavefront's chunks of the piece: lookups + MFMA
-    float4_t pacc = {0.f, 0.f, 0.f, 0.f};
-    for (int s0 = 0; s0 < CPW8; s0 += kRing) {
-#pragma unroll
-      for (int r = 0; r < kRing; ++r) {
-        const int s = s0 + r;
-        int64_t c;
-        const bool ok = slot_chunk(p, s, c);
-        cvec w;
-        if (ok) w = ring[r];
-        // prefetch the slot 8 ahead (possibly in the next piece)
-        {
-          int np = p, ns = s + kRing;
-          if (ns >= CPW8) {
-            ns -= CPW8;
-            ++np;
-          }
-          int64_t nc;
-          if (np < plan.npieces && slot_chunk(np, ns, nc))
-            ring[r] = *reinterpret_cast<const cvec*>(tile_codes + nc * 64 * GB);
-        }
-        if (ok) {
-          uint32_t sel[8];
-          selectors<BITS>(w, sel);
-          half2_t s_lo, s_hi;
-          if (MODE == 1) {
-            const half2_t sc2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sbase[c * 64], 1.0f, false);
-            s_lo = half2_t{sc2[0], sc2[0]};
-            s_hi = half2_t{sc2[1], sc2[1]};
-          }
-          const int cl = (int)(c - (int64_t)p * PK);
-#pragma unroll
-          for (int st = 0; st < 4; ++st) {
-            uint32_t a0, a1, a2, a3;
-            lookup4(sel[2 * st], tl0, tl1, th0, th1, a0, a1);
-            lookup4(sel[2 * st + 1], tl0, tl1, th0, th1, a2, a3);
-            half8_t af = as_half8(a0, a1, a2, a3);
-            if (MODE == 1) af = scale_half8(af, st < 2 ? s_lo : s_hi);
-            half8_t bf = half8_t{};
-            if (xlane) bf = *reinterpret_cast<const half8_t*>(xs + j * rowstride + cl * 128 + 32 * q + 8 * st);
-            pacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf, pacc, 0, 0, 0);
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int r2 = 0; r2 < 4; ++r2) acc[r2] += pacc[r2] * unscale;
-    __syncthreads();   // the piece buffer is free again
   }
-
-  // ---- 5. reduce the KS partial sums of each row tile (fixed order) and store
-  if (MODE == 1) {
-    const float g = *Gp;
-#pragma unroll
-    for (int r2 = 0; r2 < 4; ++r2) acc[r2] *= g;
-  }
-  float4_t* red = reinterpret_cast<float4_t*>(smem);
-  red[wave * 64 + lane] = acc;
-  __syncthreads();
   if (ks == 0 && tile_ok && xlane) {
     for (int k2 = 1; k2 < KS; ++k2) {
       const float4_t o = red[(wave + k2) * 64 + lane];
@@ -299,6 +321,7 @@ __global__ __launch_bounds__(512) void lut_gemv_kernel(const uint16_t* __restric
       acc[2] += o[2];
       acc[3] += o[3];
     }
+    const int q = lane >> 4, j = lane & 15;
 #pragma unroll
     for (int r2 = 0; r2 < 4; ++r2) {
       const int64_t row = tile * 16 + 4 * q + r2;
@@ -313,33 +336,320 @@ __global__ __launch_bounds__(512) void lut_gemv_kernel(const uint16_t* __restric
   }
 }
 
+constexpr int kRingSingle = 4;
+constexpr int kRingMulti = 8;
+
+// ---------------------------------------------------------------- single piece
+// LDS: B staged rows of (KC + 1) * 128 + 8 fp16 (the last chunk of each row is
+// zero, 8 elements of padding stagger the rows over the banks), then W * 1 KiB
+// for the K-split reduction.
+template <int BITS, int MODE>
+__global__ __launch_bounds__(1024) void lut_gemv_single_kernel(const uint16_t* __restrict__ x, int B, int64_t K,
+                                                               const uint8_t* __restrict__ codes,
+                                                               const uint16_t* __restrict__ lut,
+                                                               const uint8_t* __restrict__ scales,
+                                                               const float* __restrict__ Gp, int64_t N,
+                                                               GemvPlan plan, int out_kind, void* __restrict__ y) {
+  constexpr int RING = kRingSingle;
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int lane = threadIdx.x & 63;
+  // wavefront index as a uniform value: the LDS address of the direct loads
+  // (M0) and all slot bookkeeping stay scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nthreads = blockDim.x, W = nthreads >> 6;
+  const int KS = plan.KS, rt = wave / KS, ks = wave % KS;
+  const int64_t tile = (int64_t)blockIdx.x * plan.RT + rt;
+  const bool tile_ok = tile < plan.tiles;
+  const int64_t tile_c = tile_ok ? tile : plan.tiles - 1;
+  const int KCi = (int)plan.KC;
+  const int rowstride = (KCi + 1) * 128 + 8;
+  _Float16* xs = reinterpret_cast<_Float16*>(smem);
+  float4_t* red = reinterpret_cast<float4_t*>(smem + (size_t)B * rowstride * 2);
+  __shared__ uint32_t pmax[16];
+
+  if ((int)threadIdx.x < 16) pmax[threadIdx.x] = 0u;
+  for (int t = threadIdx.x; t < B * 16; t += nthreads)   // zero chunk of every staged row
+    reinterpret_cast<uint4_t*>(xs + (t >> 4) * rowstride + KCi * 128)[t & 15] = uint4_t{0u, 0u, 0u, 0u};
+
+  // ---- 1. lookup table (lane: row lane % 16 of the tile), and the raw bf16
+  // activations straight into LDS: one wavefront load per 128-element chunk
+  // (lane l: elements 2l, 2l+1; the clamped tail past K is zeroed below)
+  const int i = lane & 15, j = lane & 15, q = lane >> 4;
+  uint4_t tab{0u, 0u, 0u, 0u};
+  if (tile_ok) tab = load_table<BITS>(MODE == 0 ? lut + (tile * 16 + i) * (1 << BITS) : lut);
+  for (int jj = 0; jj < B; ++jj)
+    for (int c = wave; c < KCi; c += W) {
+      const int64_t k = min((int64_t)c * 128 + 2 * lane, K - 2);
+      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(x + (int64_t)jj * K + k),
+                                       reinterpret_cast<void*>(xs + jj * rowstride + c * 128), 4, 0, 0);
+    }
+  __builtin_amdgcn_s_waitcnt((0 & 0xF) | (0x7 << 4) | (0xF << 8));   // vmcnt(0): activations in LDS
+  __syncthreads();
+
+  // ---- 2. per-row maxima, then fp16 in place.  A 16-lane group covers 16
+  // consecutive vectors of one batch row (vpr is a multiple of 16).  The row
+  // index f / vpr is exact through fp32: f + 0.5 lies at least 0.5 / vpr away
+  // from a multiple of vpr, far above the rounding error for f < 2^22.
+  const int vpr = KCi * 16, nvec = B * vpr;
+  const float rvpr = 1.0f / (float)vpr;
+  for (int base = wave * 64; base < nvec; base += nthreads) {
+    const int f = base + lane;
+    const int jj = (int)(((float)f + 0.5f) * rvpr), pos = f - jj * vpr;
+    float m = 0.0f;
+    if (f < nvec && (int64_t)pos * 8 < K) m = max_abs8(*reinterpret_cast<const uint4_t*>(xs + jj * rowstride + pos * 8));
+    m = group16_max(m);
+    if ((lane & 15) == 0 && m > 0.0f) atomicMax(&pmax[jj], __float_as_uint(m));
+  }
+  __syncthreads();
+  for (int base = wave * 64; base < nvec; base += nthreads) {
+    const int f = base + lane;
+    if (f < nvec) {
+      const int jj = (int)(((float)f + 0.5f) * rvpr), pos = f - jj * vpr;
+      uint4_t* slot = reinterpret_cast<uint4_t*>(xs + jj * rowstride + pos * 8);
+      const half8_t h = (int64_t)pos * 8 < K ? to_half8_scaled(*slot, __builtin_ldexpf(1.0f, stage_exponent(pmax[jj])))
+                                             : half8_t{};
+      *reinterpret_cast<half8_t*>(slot) = h;
+    }
+  }
+  __syncthreads();
+  const bool xlane = j < B;
+  const float unscale = xlane ? __builtin_ldexpf(1.0f, -stage_exponent(pmax[j])) : 1.0f;
+
+  // ---- 3. the first RING code loads, once the activations are staged: while
+  // every compute unit starts its weight stream, issuing a load can stall on
+  // back-pressure, which must not hold up the staging barriers
+  CodeStream<BITS, MODE, RING> cs;
+  cs.init(codes + tile_c * plan.KC * CodeStream<BITS, MODE, RING>::kChunkBytes,
+          MODE == 1 ? scales + tile_c * plan.KC * 128 : nullptr, lane, KCi, KS, ks, KCi);
+#pragma unroll
+  for (int r = 0; r < RING; ++r) cs.load(r, cs.chunk(0, r));
+
+  // ---- 4. slots
+  float4_t pacc[4];
+#pragma unroll
+  for (int st = 0; st < 4; ++st) pacc[st] = float4_t{0.f, 0.f, 0.f, 0.f};
+  // batch columns >= B read row 0: their MFMA output columns are never stored
+  const _Float16* xrow = xs + (xlane ? j : 0) * rowstride + 32 * q;
+  consume<BITS, MODE, RING>(cs, 0, 0, plan.CPW, xrow, tile_ok ? 0 : KCi, tab, pacc);
+  float4_t acc;
+#pragma unroll
+  for (int r2 = 0; r2 < 4; ++r2) acc[r2] = ((pacc[0][r2] + pacc[1][r2]) + (pacc[2][r2] + pacc[3][r2])) * unscale;
+  if (MODE == 1) {
+    const float g = *Gp;
+#pragma unroll
+    for (int r2 = 0; r2 < 4; ++r2) acc[r2] *= g;
+  }
+  // ---- 5. K-split reduction and store
+  reduce_store(acc, red, wave, lane, ks, KS, tile_ok, tile, N, out_kind, y, xlane);
+}
+
+// ---------------------------------------------------------------- several pieces
+template <int BITS, int MODE>
+__global__ __launch_bounds__(768) void lut_gemv_multi_kernel(const uint16_t* __restrict__ x, int B, int64_t K,
+                                                             const uint8_t* __restrict__ codes,
+                                                             const uint16_t* __restrict__ lut,
+                                                             const uint8_t* __restrict__ scales,
+                                                             const float* __restrict__ Gp, int64_t N,
+                                                             GemvPlan plan, int out_kind, void* __restrict__ y) {
+  constexpr int RING = kRingMulti;
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nthreads = blockDim.x;
+  const int KS = plan.KS, rt = wave / KS, ks = wave % KS;
+  const int64_t tile = (int64_t)blockIdx.x * plan.RT + rt;
+  const bool tile_ok = tile < plan.tiles;
+  const int64_t tile_c = tile_ok ? tile : plan.tiles - 1;
+  const int PK = plan.PK, NP = plan.npieces;
+  const int vpr = PK * 16;                         // 8-element vectors per staged piece row
+  const int rowstride = (PK + 1) * 128 + 8;        // fp16 elements per staged batch row (+ zero chunk, pad)
+  _Float16* xs = reinterpret_cast<_Float16*>(smem);
+  float4_t* red = reinterpret_cast<float4_t*>(smem + (size_t)B * rowstride * 2);
+  __shared__ uint32_t piece_max[2][16];            // double-buffered per-piece batch-row maxima
+
+  // Staging assignment, fixed for the kernel: vector n of this thread is
+  // elements [8*spos, 8*spos + 8) of batch row sj of every piece (valid when
+  // sj < B); the division is exact as in the single-piece kernel.
+  int sj[kStageVec], spos[kStageVec];
+  {
+    const float rvpr = 1.0f / (float)vpr;
+#pragma unroll
+    for (int n = 0; n < kStageVec; ++n) {
+      const int f = n * nthreads + (int)threadIdx.x;
+      sj[n] = (int)(((float)f + 0.5f) * rvpr);
+      spos[n] = f - sj[n] * vpr;
+    }
+  }
+  uint4_t v[kStageVec];
+  auto load_piece_x = [&](int p) {
+    const int64_t k0 = (int64_t)p * PK * 128;
+#pragma unroll
+    for (int n = 0; n < kStageVec; ++n) {
+      const bool ok = sj[n] < B;
+      int64_t k = k0 + (int64_t)spos[n] * 8;
+      const bool in_k = ok && k < K;
+      k = in_k ? k : 0;
+      const uint4_t t = *reinterpret_cast<const uint4_t*>(x + (int64_t)(ok ? sj[n] : 0) * K + k);   // in bounds
+      v[n] = in_k ? t : uint4_t{0u, 0u, 0u, 0u};
+    }
+  };
+  if ((int)threadIdx.x < 16) {
+    piece_max[0][threadIdx.x] = 0u;
+    piece_max[1][threadIdx.x] = 0u;
+  }
+  for (int t = threadIdx.x; t < B * 16; t += nthreads)   // zero chunk of every staged row
+    reinterpret_cast<uint4_t*>(xs + (t >> 4) * rowstride + PK * 128)[t & 15] = uint4_t{0u, 0u, 0u, 0u};
+
+  // ---- 1. lookup table, the first activation piece and this workgroup's
+  // share of the L2 warm-up of the whole activation matrix (workgroup b runs
+  // on XCD b % 8)
+  const int i = lane & 15, q = lane >> 4, j = lane & 15;
+  uint4_t tab{0u, 0u, 0u, 0u};
+  if (tile_ok) tab = load_table<BITS>(MODE == 0 ? lut + (tile * 16 + i) * (1 << BITS) : lut);
+  load_piece_x(0);
+  uint32_t warm = 0;
+  {
+    const uint32_t V = (uint32_t)(B * K / 8);      // 16-byte vectors of x
+    const uint32_t wgs_xcd = (gridDim.x + 7) / 8, share = (V + wgs_xcd - 1) / wgs_xcd;
+    const uint32_t lo = (blockIdx.x / 8) * share, hi = min(V, lo + share);
+    for (uint32_t f = lo + threadIdx.x; f < hi; f += nthreads) warm ^= reinterpret_cast<const uint4_t*>(x)[f][0];
+  }
+
+  CodeStream<BITS, MODE, RING> cs;
+  cs.init(codes + tile_c * plan.KC * CodeStream<BITS, MODE, RING>::kChunkBytes,
+          MODE == 1 ? scales + tile_c * plan.KC * 128 : nullptr, lane, PK, KS, ks, (int)plan.KC);
+  const bool xlane = j < B;
+  float4_t acc = {0.f, 0.f, 0.f, 0.f};
+
+  for (int p = 0; p < NP; ++p) {
+    // ---- 2. stage the activation piece: maxima, then fp16
+    uint32_t* pm = piece_max[p & 1];
+#pragma unroll
+    for (int n = 0; n < kStageVec; ++n) {
+      const float m = group16_max(max_abs8(v[n]));
+      if ((lane & 15) == 0 && sj[n] < B && m > 0.0f) atomicMax(&pm[sj[n]], __float_as_uint(m));
+    }
+    if (p == 0) asm volatile("" ::"v"(warm));      // the warm-up loads have landed
+    __syncthreads();
+#pragma unroll
+    for (int n = 0; n < kStageVec; ++n)
+      if (sj[n] < B)
+        *reinterpret_cast<half8_t*>(xs + sj[n] * rowstride + spos[n] * 8) =
+            to_half8_scaled(v[n], __builtin_ldexpf(1.0f, stage_exponent(pm[sj[n]])));
+    if ((int)threadIdx.x < 16) piece_max[(p + 1) & 1][threadIdx.x] = 0u;   // last read in piece p-1
+    __syncthreads();
+    const float unscale = xlane ? __builtin_ldexpf(1.0f, -stage_exponent(pm[j])) : 1.0f;
+    if (p == 0) {
+      // ---- 3. the first RING code loads, once the first piece is staged (a
+      // load issued while the weight streams start can stall on back-pressure)
+#pragma unroll
+      for (int r = 0; r < RING; ++r) cs.load(r, cs.chunk(0, r));
+    }
+    load_piece_x(min(p + 1, NP - 1));              // L2 hits (warmed above); the last piece re-reads itself
+
+    // ---- 4. this wavefront's slots of the piece
+    float4_t pacc[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) pacc[st] = float4_t{0.f, 0.f, 0.f, 0.f};
+    const _Float16* xrow = xs + (xlane ? j : 0) * rowstride + 32 * q;
+    consume<BITS, MODE, RING>(cs, p, min(p + 1, NP - 1), plan.CPW, xrow, tile_ok ? 0 : PK, tab, pacc);
+#pragma unroll
+    for (int r2 = 0; r2 < 4; ++r2) acc[r2] += ((pacc[0][r2] + pacc[1][r2]) + (pacc[2][r2] + pacc[3][r2])) * unscale;
+    __syncthreads();   // the piece buffer is free again
+  }
+  if (MODE == 1) {
+    const float g = *Gp;
+#pragma unroll
+    for (int r2 = 0; r2 < 4; ++r2) acc[r2] *= g;
+  }
+  // ---- 5. K-split reduction and store
+  reduce_store(acc, red, wave, lane, ks, KS, tile_ok, tile, N, out_kind, y, xlane);
+}
+
+__global__ void zero_fill_kernel(uint32_t* p, int64_t n) {
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < n; t += (int64_t)gridDim.x * blockDim.x) p[t] = 0u;
+}
+
+constexpr int64_t kLdsPerCu = 160 * 1024;
+constexpr int64_t kSingleLdsMax = 148 * 1024;   // staged activations of the single-piece kernel
+constexpr int kCUs = 256;
+
 template <int BITS, int MODE>
 hipError_t launch_gemv_t(const uint16_t* x, int64_t B, const LutView& w, int out_kind, void* y, hipStream_t s) {
   const int64_t N = w.rows, K = w.cols;
   GemvPlan pl{};
   pl.tiles = round_up(N, 16) / 16;
   pl.KC = round_up(K, 128) / 128;
-  // about 8 chunks per wavefront, at most 8 wavefronts per workgroup
-  pl.KS = (int)std::min<int64_t>(8, std::max<int64_t>(1, (pl.KC + 7) / 8));
-  int64_t rt = pl.tiles / 256;
-  pl.RT = (int)std::max<int64_t>(1, std::min<int64_t>(rt, 8 / pl.KS));
+  const int64_t lds_single = B * ((pl.KC + 1) * 128 + 8) * 2;
+  if (lds_single <= kSingleLdsMax) {
+    // Single piece.  Measured on the decode shapes: the best splits put
+    // about 12 wavefronts per compute unit in all (KS ~ 3072 / tiles K-splits
+    // per row tile), with a K-split that wastes few ring slots, and 2-3 row
+    // tiles per workgroup so that the activation staging is shared, while
+    // keeping at least one workgroup per compute unit where the row tiles
+    // allow it.
+    const int64_t ks0 = std::min<int64_t>(std::min<int64_t>(16, pl.KC), std::max<int64_t>(1, (3072 + pl.tiles - 1) / pl.tiles));
+    double best = 1e300;
+    for (int64_t ks = std::max<int64_t>(1, ks0 - 3); ks <= std::min<int64_t>(std::min<int64_t>(16, pl.KC), ks0 + 3); ++ks)
+      for (int rt = 3; rt >= 1; --rt) {
+        if (rt * ks > 16) continue;
+        const int64_t cpw = round_up((pl.KC + ks - 1) / ks, kRingSingle);
+        const int64_t G = (pl.tiles + rt - 1) / rt;
+        double score = (double)(cpw * ks) / (double)pl.KC;               // slot waste
+        score *= 1.0 + 0.05 * (double)std::abs(ks - ks0);                 // distance from the wavefront target
+        if (rt == 1) score *= 1.3;                                        // staging not shared
+        if (G < kCUs && rt > 1) score *= 1.0 + 0.3 * (1.0 - (double)G / kCUs);   // idle compute units
+        // workgroups that fit one compute unit's LDS at once: a partial extra
+        // round of workgroups costs a whole one
+        const int64_t slots = kCUs * std::max<int64_t>(1, kLdsPerCu / (lds_single + rt * ks * 1024));
+        if (G > slots) score *= (double)((G + slots - 1) / slots) / ((double)G / (double)slots);
+        if (score < best * 0.999) {
+          best = score;
+          pl.RT = rt;
+          pl.KS = (int)ks;
+          pl.CPW = (int)cpw;
+        }
+      }
+    pl.PK = (int)pl.KC;
+    pl.npieces = 1;
+    const int W = pl.RT * pl.KS;
+    const size_t lds = (size_t)lds_single + (size_t)W * 1024;
+    const int64_t blocks = (pl.tiles + pl.RT - 1) / pl.RT;
+    hipLaunchKernelGGL((lut_gemv_single_kernel<BITS, MODE>), dim3((unsigned)blocks), dim3(W * 64), lds, s, x,
+                       (int)B, K, w.codes, w.lut, w.scales, w.G, N, pl, out_kind, y);
+    return hipGetLastError();
+  }
+  // Several pieces.  Row tiles per workgroup: the workgroups must spread
+  // evenly over the compute units (cost = rounds x row tiles per workgroup);
+  // ties go to more row tiles per workgroup, which amortizes the staging.  K
+  // splits per row tile: about 8 chunks per wavefront, at most 12 wavefronts.
+  const int64_t ks0 = std::max<int64_t>(1, (pl.KC + 7) / 8);
+  int best_rt = 1;
+  int64_t best_cost = INT64_MAX;
+  for (int rt = 1; rt <= 12; ++rt) {
+    const int64_t wgs = (pl.tiles + rt - 1) / rt;
+    const int64_t cost = ((wgs + kCUs - 1) / kCUs) * rt;
+    if (cost <= best_cost) {
+      best_cost = cost;
+      best_rt = rt;
+    }
+  }
+  pl.RT = best_rt;
+  pl.KS = (int)std::min<int64_t>(ks0, std::max(1, 12 / pl.RT));
   const int W = pl.RT * pl.KS;
   const int nthreads = W * 64;
-  // piece: activations in LDS (<= 64 KiB) and at most kStageVec 8-vectors per thread
+  // piece: activations in LDS (<= 64 KiB with the zero chunk) and at most
+  // kStageVec 8-vectors per thread
+  auto lds_x = [&](int64_t pk) { return B * ((pk + 1) * 128 + 8) * 2; };
   int64_t pk = pl.KC;
-  while (pk > 1 && ((int64_t)B * (pk * 128 + 8) * 2 > 64 * 1024 || B * pk * 16 > (int64_t)kStageVec * nthreads))
-    pk = (pk + 1) / 2;
+  while (pk > 1 && (lds_x(pk) > 64 * 1024 || B * pk * 16 > (int64_t)kStageVec * nthreads)) pk = (pk + 1) / 2;
   pl.PK = (int)pk;
   pl.npieces = (int)((pl.KC + pk - 1) / pk);
-  const int cpw = (int)((pk + pl.KS - 1) / pl.KS);
-  pl.CPW8 = (cpw + kRing - 1) / kRing * kRing;
-  size_t lds = (size_t)B * (pk * 128 + 8) * 2;
-  const size_t red = (size_t)W * 64 * 16;
-  if (lds < red) lds = red;
-  auto kern = lut_gemv_kernel<BITS, MODE>;
+  pl.CPW = (int)round_up((pk + pl.KS - 1) / pl.KS, kRingMulti);
+  const size_t lds = (size_t)lds_x(pk) + (size_t)W * 1024;
   const int64_t blocks = (pl.tiles + pl.RT - 1) / pl.RT;
-  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(nthreads), lds, s, x, (int)B, K, w.codes, w.lut, w.scales,
-                     w.G, N, pl, out_kind, y);
+  hipLaunchKernelGGL((lut_gemv_multi_kernel<BITS, MODE>), dim3((unsigned)blocks), dim3(nthreads), lds, s, x, (int)B,
+                     K, w.codes, w.lut, w.scales, w.G, N, pl, out_kind, y);
   return hipGetLastError();
 }
 
@@ -348,6 +658,12 @@ hipError_t launch_gemv_t(const uint16_t* x, int64_t B, const LutView& w, int out
 hipError_t launch_gemv(const uint16_t* x, int64_t B, const LutView& w, int out_kind, void* y,
                        hipStream_t s) {
   if (w.rows == 0 || B == 0) return hipSuccess;
+  if (w.cols == 0) {   // empty sum: y = 0 (fp32 or bf16 zeros are all-zero bits)
+    const int64_t words = (B * w.rows * (out_kind == 0 ? 4 : 2) + 3) / 4;
+    hipLaunchKernelGGL(zero_fill_kernel, dim3((unsigned)std::min<int64_t>(1024, (words + 255) / 256)), dim3(256), 0, s,
+                       reinterpret_cast<uint32_t*>(y), words);
+    return hipGetLastError();
+  }
   if (w.bits == 3)
     return w.mode == 0 ? launch_gemv_t<3, 0>(x, B, w, out_kind, y, s)
                        : launch_gemv_t<3, 1>(x, B, w, out_kind, y, s);
