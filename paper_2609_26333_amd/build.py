@@ -19,8 +19,9 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdq.so")
 
 ARCH = "gfx950"
-# Quantizers must round exactly as written: no contraction of a*b+c.
-EXACT_TUS = {"quant.hip", "pack_lut.hip"}
+# Quantizers (and the GEMM's requantizing epilogue) must round exactly as
+# written: no contraction of a*b+c.
+EXACT_TUS = {"quant.hip", "pack_lut.hip", "gemm.hip"}
 SOURCES = ["quant.hip", "pack_lut.hip", "gemm.hip", "gemv.hip", "dq_api.cpp"]
 
 

@@ -199,19 +199,25 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
     if (!aligned(X, 16)) return fail(DQ_ERR_INVALID_ARG, "X must be 16-byte aligned");
   }
   if (epilogue_flags & ~DQ_EPI_SWIGLU) return fail(DQ_ERR_INVALID_ARG, "unknown epilogue flag");
+  const bool swiglu = (epilogue_flags & DQ_EPI_SWIGLU) != 0;
+  if (swiglu && N % 32 != 0) return fail(DQ_ERR_INVALID_ARG, "SwiGLU needs W rows %% 32 == 0 (gate/up groups of 16)");
+  const int64_t Nout = swiglu ? N / 2 : N;
   if (out_kind != DQ_OUT_F32 && out_kind != DQ_OUT_BF16 && out_kind != DQ_OUT_NVFP4)
     return fail(DQ_ERR_INVALID_ARG, "bad out_kind");
   if (out_kind == DQ_OUT_NVFP4) {
     if (Y != nullptr) return fail(DQ_ERR_INVALID_ARG, "NVFP4 output: Y must be NULL");
     if (G_out_static == nullptr || !aligned(G_out_static, 4))
       return fail(DQ_ERR_INVALID_ARG, "NVFP4 output needs an aligned G_out_static");
+    if (Yq == nullptr) return fail(DQ_ERR_INVALID_ARG, "NVFP4 output needs Yq");
+    if (Nout % 16 != 0) return fail(DQ_ERR_INVALID_ARG, "NVFP4 output needs output columns %% 16 == 0");
+    st = check_nvfp4(Yq, "Yq", M, Nout);
+    if (st != DQ_OK) return st;
   } else {
-    if (Y == nullptr && M * N > 0) return fail(DQ_ERR_INVALID_ARG, "Y is NULL");
+    if (Yq != nullptr) return fail(DQ_ERR_INVALID_ARG, "Yq is only used with NVFP4 output");
+    if (Y == nullptr && M * Nout > 0) return fail(DQ_ERR_INVALID_ARG, "Y is NULL");
     if (!aligned(Y, 16)) return fail(DQ_ERR_INVALID_ARG, "Y must be 16-byte aligned");
   }
   if (X != nullptr) return fail(DQ_ERR_UNSUPPORTED, "fused activation quantization is not built yet");
-  if (out_kind == DQ_OUT_NVFP4 || epilogue_flags != 0)
-    return fail(DQ_ERR_UNSUPPORTED, "NVFP4 / SwiGLU epilogues are not built yet");
   dq::GemmArgs a{};
   if (A) a.A = view(A);
   a.X = X;

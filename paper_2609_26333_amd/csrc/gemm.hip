@@ -150,11 +150,36 @@ __device__ inline void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-template <int WN, int NBW, int KS, int OUT>
+// Output side of the GEMM: the plain result (fp32 / bf16, [M, Nout]) or its
+// NVFP4 requantization (the next layer's input) in the tiled layout of dq.h.
+struct GemmOut {
+  void* Y;                 // OUT_F32 / OUT_BF16
+  const float* G_out;      // OUT_NVFP4: static scale of the next layer's input
+  uint8_t* codes;          // OUT_NVFP4
+  uint8_t* scales;
+  float* G;                // receives *G_out (may alias it)
+  int64_t Nout;            // N, or N / 2 with SwiGLU
+  int64_t tiles_r, tiles_c;   // NVFP4 tiles of [M, Nout]
+};
+
+enum { kOutF32 = 0, kOutBF16 = 1, kOutNvfp4 = 2 };
+
+// silu(g) * u in fp32 (SwiGLU, the MLP non-linearity between gate/up and down)
+__device__ inline float swiglu(float g, float u) { return g / (1.0f + expf(-g)) * u; }
+
+// One E2M1 code (low nibble) of v for the block scale S != 0: the same
+// arithmetic as the activation quantizer (correctly rounded v / S, hardware
+// round-to-nearest-even with saturation, +0 for magnitude zero).
+__device__ inline uint32_t e2m1_code(float v, float S) {
+  const float rcp = 1.0f / S;
+  return fp4_canonical_zero(cvt_pk_fp4<0>(0u, div_by_scale(v, S, rcp), 0.0f)) & 0xFu;
+}
+
+template <int WN, int NBW, int KS, int OUT, bool SW>
 __global__ __launch_bounds__(64 * 2 * WN, 1) void nvfp4_gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales, const float* __restrict__ Ga,
     const uint8_t* __restrict__ w_codes, const uint8_t* __restrict__ w_scales, const float* __restrict__ Gw,
-    int64_t M, int64_t N, int64_t a_tiles_r, int64_t w_tiles_r, int64_t KT, void* __restrict__ Y,
+    int64_t M, int64_t N, int64_t a_tiles_r, int64_t w_tiles_r, int64_t KT, GemmOut out,
     int64_t tiles_m, int64_t tiles_n) {
   typedef Geo<WN, NBW, KS> Gm;
   constexpr int kStages = Gm::stages;
@@ -259,21 +284,76 @@ __global__ __launch_bounds__(64 * 2 * WN, 1) void nvfp4_gemm_kernel(
   const float g = (*Ga) * (*Gw);
   const int col_in = lane & 31;
   const int row_off = 4 * (lane >> 5);
+  // Accumulator block (i, j): rows m0 + 32i + 8(r/4) + row_off + r%4 (r =
+  // register 0..15), GEMM column n0 + 32j + col_in.  With SwiGLU the weight
+  // rows come in gate/up groups of 16, so the gate lanes (col_in < 16) pair
+  // with the up lanes col_in + 16 and produce output feature
+  // (n0 + 32j) / 2 + col_in.
+  if constexpr (OUT != kOutNvfp4) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 4; ++i) {
 #pragma unroll
-    for (int j = 0; j < NBW; ++j) {
-      const int64_t col = n0 + j * 32 + col_in;
-      if (col >= N) continue;
+      for (int j = 0; j < NBW; ++j) {
+        const int64_t gcol = n0 + j * 32 + col_in;
+        const int64_t col = SW ? (n0 + j * 32) / 2 + col_in : gcol;
+        const bool col_ok = SW ? (col_in < 16 && col < out.Nout) : gcol < N;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + i * 32 + 8 * (r >> 2) + row_off + (r & 3);
-        if (row < M) {
-          const float v = acc[i][j][r] * g;
-          if (OUT == 0)
-            reinterpret_cast<float*>(Y)[row * N + col] = v;
-          else
-            reinterpret_cast<uint16_t*>(Y)[row * N + col] = (uint16_t)f32_to_bf16_rne(v);
+        for (int r = 0; r < 16; ++r) {
+          const int64_t row = m0 + i * 32 + 8 * (r >> 2) + row_off + (r & 3);
+          float v = acc[i][j][r] * g;
+          if (SW) v = swiglu(v, __shfl_xor(v, 16, 64));
+          if (col_ok && row < M) {
+            if (OUT == kOutF32)
+              reinterpret_cast<float*>(out.Y)[row * out.Nout + col] = v;
+            else
+              reinterpret_cast<uint16_t*>(out.Y)[row * out.Nout + col] = (uint16_t)f32_to_bf16_rne(v);
+          }
+        }
+      }
+    }
+  } else {
+    // NVFP4 requantization along the output columns (the next layer's K):
+    // a 16-lane group holds one 16-block of one row, so the block maximum is
+    // four cross-lane steps; 8 lanes pack their codes into one dword.
+    const float Go = *out.G_out;
+    const float den = 6.0f * Go;
+    if (blockIdx.x == 0 && threadIdx.x == 0 && out.G != out.G_out) *out.G = Go;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t tr = (m0 + i * 32) / 32;
+      if (tr >= out.tiles_r) continue;
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) {
+        const int64_t gcol = n0 + j * 32 + col_in;
+        const int64_t cbase = SW ? (n0 + j * 32) / 2 : n0 + j * 32;   // first output column of the block
+        const int64_t tc = cbase / 64;
+        if (tc >= out.tiles_c) continue;
+        const int64_t col = cbase + col_in;
+        const bool writer = SW ? col_in < 16 : true;
+        const bool col_ok = writer && col < out.Nout && gcol < N;
+        const int cc = (int)(col & 63);
+        uint8_t* tcodes = out.codes + (tr * out.tiles_c + tc) * 1024;
+        uint8_t* tscales = out.scales + (tr * out.tiles_c + tc) * 128;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int rr = 8 * (r >> 2) + row_off + (r & 3);
+          const int64_t row = tr * 32 + rr;
+          float v = acc[i][j][r] * g;
+          if (SW) v = swiglu(v, __shfl_xor(v, 16, 64));
+          if (!(col_ok && row < M)) v = 0.0f;    // padding of the tile: zero codes and scales
+          float a = fabsf(v);
+          a = fmaxf(a, __shfl_xor(a, 1, 64));
+          a = fmaxf(a, __shfl_xor(a, 2, 64));
+          a = fmaxf(a, __shfl_xor(a, 4, 64));
+          a = fmaxf(a, __shfl_xor(a, 8, 64));
+          const uint32_t c = e4m3_encode_rne_sat(a / den);
+          const float S = e4m3_decode(c) * Go;
+          uint32_t w = (S == 0.0f ? 0u : e2m1_code(v, S)) << (4 * (lane & 7));
+          w |= __shfl_xor(w, 1, 64);
+          w |= __shfl_xor(w, 2, 64);
+          w |= __shfl_xor(w, 4, 64);
+          if (writer && (lane & 7) == 0) *reinterpret_cast<uint32_t*>(tcodes + rr * 32 + cc / 2) = w;
+          if (writer && (lane & 15) == 0) tscales[rr * 4 + cc / 16] = (uint8_t)c;
         }
       }
     }
@@ -288,19 +368,44 @@ hipError_t launch_geo(const GemmArgs& a, hipStream_t s) {
   const int64_t KT = round_up(a.K, 64) / 64;
   const int64_t tiles_m = (a.M + kBlkM - 1) / kBlkM, tiles_n = (a.N + Gm::bn - 1) / Gm::bn;
   const size_t lds = (size_t)Gm::stages * Gm::bytes;
-  auto kern = a.out_kind == 0 ? nvfp4_gemm_kernel<WN, NBW, KS, 0> : nvfp4_gemm_kernel<WN, NBW, KS, 1>;
+  const bool sw = (a.flags & 1) != 0;
+  GemmOut o{};
+  o.Y = a.Y;
+  o.Nout = sw ? a.N / 2 : a.N;
+  if (a.out_kind == kOutNvfp4) {
+    o.G_out = a.G_out;
+    o.codes = a.Yq.codes;
+    o.scales = a.Yq.scales;
+    o.G = a.Yq.G;
+    o.tiles_r = round_up(a.M, 32) / 32;
+    o.tiles_c = round_up(o.Nout, 64) / 64;
+  }
+  typedef void (*kern_t)(const uint8_t*, const uint8_t*, const float*, const uint8_t*, const uint8_t*, const float*,
+                         int64_t, int64_t, int64_t, int64_t, int64_t, GemmOut, int64_t, int64_t);
+  static const kern_t kerns[3][2] = {
+      {nvfp4_gemm_kernel<WN, NBW, KS, kOutF32, false>, nvfp4_gemm_kernel<WN, NBW, KS, kOutF32, true>},
+      {nvfp4_gemm_kernel<WN, NBW, KS, kOutBF16, false>, nvfp4_gemm_kernel<WN, NBW, KS, kOutBF16, true>},
+      {nvfp4_gemm_kernel<WN, NBW, KS, kOutNvfp4, false>, nvfp4_gemm_kernel<WN, NBW, KS, kOutNvfp4, true>}};
+  const kern_t kern = kerns[a.out_kind][sw ? 1 : 0];
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_m * tiles_n)), dim3(Gm::threads), lds, s, a.A.codes, a.A.scales,
-                     a.A.G, a.W.codes, a.W.scales, a.W.G, a.M, a.N, a_tiles_r, w_tiles_r, KT, a.Y, tiles_m, tiles_n);
+                     a.A.G, a.W.codes, a.W.scales, a.W.G, a.M, a.N, a_tiles_r, w_tiles_r, KT, o, tiles_m, tiles_n);
   return hipGetLastError();
 }
 
 }  // namespace
 
+__global__ void publish_scale_kernel(const float* src, float* dst) { *dst = *src; }
+
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
-  if (a.M == 0 || a.N == 0) return hipSuccess;
+  if (a.M == 0 || a.N == 0) {
+    // empty result: an NVFP4 output still carries its scale
+    if (a.out_kind == kOutNvfp4 && a.Yq.G != a.G_out)
+      hipLaunchKernelGGL(publish_scale_kernel, dim3(1), dim3(1), 0, s, a.G_out, a.Yq.G);
+    return hipGetLastError();
+  }
   // 256x256 workgroup tiles as 2x4 wavefronts of 128x64 (two wavefronts per
   // SIMD hide each other's LDS / barrier / load stalls).
   return launch_geo<4, 2, 2>(a, s);

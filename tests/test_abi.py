@@ -86,6 +86,33 @@ def test_invalid_arguments_rejected_on_host():
                                None) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w), 4, 0, fake, None, None, 4,
                                None) == dq.DQ_ERR_INVALID_ARG
+    # SwiGLU needs gate/up groups of 16 rows (W rows % 32 == 0)
+    w48 = _nv(48, 32, fake, fake, fake)
+    assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w48), 4, 0, fake, None, None,
+                               dq.EPI_SWIGLU, None) == dq.DQ_ERR_INVALID_ARG
+    # NVFP4 output: Y must be NULL, Yq and G_out given, Yq shaped [M, N] ([M, N/2] with SwiGLU)
+    w64 = _nv(64, 32, fake, fake, fake)
+    yq = _nv(4, 64, fake, fake, fake)
+    yq_sw = _nv(4, 32, fake, fake, fake)
+    assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w64), 4, dq.OUT_NVFP4, fake, fake,
+                               ctypes.byref(yq), 0, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w64), 4, dq.OUT_NVFP4, None, None,
+                               ctypes.byref(yq), 0, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w64), 4, dq.OUT_NVFP4, None, fake,
+                               None, 0, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w64), 4, dq.OUT_NVFP4, None, fake,
+                               ctypes.byref(yq_sw), 0, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w64), 4, dq.OUT_NVFP4, None, fake,
+                               ctypes.byref(yq), dq.EPI_SWIGLU, None) == dq.DQ_ERR_INVALID_ARG
+    # Yq with a plain output
+    assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w64), 4, 0, fake, None,
+                               ctypes.byref(yq), 0, None) == dq.DQ_ERR_INVALID_ARG
+    # NVFP4 output columns must be a multiple of 16 (here 40 / 2 = 20 after SwiGLU is refused first;
+    # 24 rows without SwiGLU)
+    w24 = _nv(24, 32, fake, fake, fake)
+    yq24 = _nv(4, 24, fake, fake, fake)
+    assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w24), 4, dq.OUT_NVFP4, None, fake,
+                               ctypes.byref(yq24), 0, None) == dq.DQ_ERR_INVALID_ARG
     # GEMV: batch out of range, bad bits
     lw = dq._Lut(fake, fake, None, None, 16, 128, 3, 0)
     assert lib.dq_decode_gemv(fake, 0, ctypes.byref(lw), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
