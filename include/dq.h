@@ -8,8 +8,9 @@
  *   offline:  dq_pack_nvfp4, dq_pack_lut3                 (weight packing)
  *
  * Conventions for every call
- *   - Buffers are device memory owned by the caller.  The library allocates
- *     nothing and keeps no state except a thread-local last-error string.
+ *   - Buffers are device memory owned by the caller.  The library keeps no
+ *     state except a thread-local last-error string, and allocates nothing
+ *     except the stream-ordered staging of dq_prefill_gemm's fused path.
  *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*;
  *     NULL is the default stream).  Nothing synchronizes inside the library.
  *   - Arguments are validated on the host before any HIP call; a rejected
@@ -178,8 +179,13 @@ dq_status dq_quantize_act_nvfp4(const uint16_t* X, int64_t M, int64_t K, const f
  * operands (exact products, fp32 accumulation).
  * A: quantized activations (rows = M, cols = K) - or NULL together with
  *   X (device bf16 [M, K]) and G_x_static (device float): the activations are
- *   then quantized inside the GEMM with the static scale (fused a1).
- *   Exactly one of A and X must be given.
+ *   then quantized with the static scale as part of this call (fused a1), by
+ *   one streaming pass into NVFP4 staging that the GEMM reads.  The staging
+ *   (M x K / 2 + M x K / 16 bytes, tile-rounded) is taken with
+ *   hipMallocAsync and released with hipFreeAsync on `stream`, so concurrent
+ *   calls on different streams do not share it; this is the only call that
+ *   allocates.  Exactly one of A and X must be given (with M == 0 the fused
+ *   call may pass X = NULL).
  * W: packed weights, rows = N, cols = K (same K as A).
  * out_kind DQ_OUT_F32 / DQ_OUT_BF16: Y is device [M, N] row-major fp32 / bf16
  *   (bf16: round to nearest even).

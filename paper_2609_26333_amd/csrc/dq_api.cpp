@@ -183,7 +183,10 @@ dq_status dq_quantize_act_nvfp4(const uint16_t* X, int64_t M, int64_t K, const f
 dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G_x_static, const dq_nvfp4_t* W,
                           int64_t M, int out_kind, void* Y, const float* G_out_static, const dq_nvfp4_t* Yq,
                           int epilogue_flags, void* stream) {
-  if ((A == nullptr) == (X == nullptr)) return fail(DQ_ERR_INVALID_ARG, "give exactly one of A and X");
+  // exactly one of A and X; an empty fused call (M == 0) may pass X = NULL
+  if (A != nullptr && X != nullptr) return fail(DQ_ERR_INVALID_ARG, "give exactly one of A and X");
+  if (A == nullptr && X == nullptr && !(M == 0 && G_x_static != nullptr))
+    return fail(DQ_ERR_INVALID_ARG, "give exactly one of A and X");
   if (W == nullptr) return fail(DQ_ERR_INVALID_ARG, "W is NULL");
   if (M < 0) return fail(DQ_ERR_INVALID_ARG, "M < 0");
   const int64_t N = W->rows, K = W->cols;
@@ -217,9 +220,28 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
     if (Y == nullptr && M * Nout > 0) return fail(DQ_ERR_INVALID_ARG, "Y is NULL");
     if (!aligned(Y, 16)) return fail(DQ_ERR_INVALID_ARG, "Y must be 16-byte aligned");
   }
-  if (X != nullptr) return fail(DQ_ERR_UNSUPPORTED, "fused activation quantization is not built yet");
   dq::GemmArgs a{};
-  if (A) a.A = view(A);
+  hipStream_t hs = (hipStream_t)stream;
+  void* staging = nullptr;
+  if (A) {
+    a.A = view(A);
+  } else {
+    // Fused activation quantization: one streaming pass of X into NVFP4
+    // staging (stream-ordered allocation), then the GEMM, then the release,
+    // all on `stream`.
+    const int64_t r = rup(M, 32), c = rup(K, 64);
+    const size_t code_bytes = (size_t)(r * c / 2), scale_bytes = (size_t)(r * c / 16);
+    const size_t bytes = code_bytes + scale_bytes + 16;
+    hipError_t e = hipMallocAsync(&staging, bytes, hs);
+    if (e != hipSuccess) return hip_status(e, "dq_prefill_gemm (staging)");
+    uint8_t* base = static_cast<uint8_t*>(staging);
+    a.A = dq::NvFp4View{base, base + code_bytes, reinterpret_cast<float*>(base + code_bytes + scale_bytes), M, K};
+    e = dq::launch_quantize_act(X, M, K, G_x_static, a.A, hs);
+    if (e != hipSuccess) {
+      (void)hipFreeAsync(staging, hs);
+      return hip_status(e, "dq_prefill_gemm (activation quantization)");
+    }
+  }
   a.X = X;
   a.G_x = G_x_static;
   a.W = view(W);
@@ -231,7 +253,12 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
   a.G_out = G_out_static;
   if (Yq) a.Yq = view(Yq);
   a.flags = epilogue_flags;
-  return hip_status(dq::launch_gemm(a, (hipStream_t)stream), "dq_prefill_gemm");
+  hipError_t e = dq::launch_gemm(a, hs);
+  if (staging != nullptr) {
+    const hipError_t f = hipFreeAsync(staging, hs);
+    if (e == hipSuccess) e = f;
+  }
+  return hip_status(e, "dq_prefill_gemm");
 }
 
 dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y, void* stream) {

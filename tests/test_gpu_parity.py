@@ -209,6 +209,64 @@ def test_gemm_end_to_end_c1_sampled_rows():
     assert err <= TOL
 
 
+FUSED_SHAPES = [(128, 512, 512), (300, 520, 1024), (1, 16, 64), (0, 32, 64)]
+
+
+@pytest.mark.parametrize("M,N,K", FUSED_SHAPES)
+def test_gemm_fused_act_quant(M, N, K):
+    """X given instead of A (fused activation quantization with a static
+    scale): the result equals quantize-then-GEMM bit for bit, and the oracle
+    within tolerance; also with the NVFP4 epilogue."""
+    say("fused", M, N, K)
+    xb = synth.random_bf16(71, (M, K), outlier_frac=0.01, outlier_factor=20)
+    calib = synth.random_bf16(1071, (max(M, 1), K), outlier_frac=0.01, outlier_factor=20)
+    G_x = nvfp4.global_scale(nvfp4.amax(formats.f32_from_bf16_bits(calib)))
+    w = synth.random_f32(72, (N, K), 0.02)
+    W = dq.dq_pack_nvfp4(dev(w))
+    Gd = dev(np.array([G_x], np.float32))
+    y_f = host(dq.dq_prefill_gemm(W, X=bf16_dev(xb), G_x_static=Gd))
+    A = dq.dq_quantize_act_nvfp4(bf16_dev(xb), G_static=Gd)
+    y_u = host(dq.dq_prefill_gemm(W, A=A))
+    assert np.array_equal(y_f, y_u)
+    if M:
+        qa, ca, _ = nvfp4.quantize_bf16_activations(xb, G_x)
+        qw, cw, Gw = nvfp4.quantize_dynamic(w)
+        assert linalg.rel_fro(y_f, linalg.nvfp4_gemm(qa, ca, G_x, qw, cw, Gw)) <= TOL
+    if N % 16 == 0:
+        G_o = dev(np.array([0.01], np.float32))
+        q_f = dq.dq_prefill_gemm(W, X=bf16_dev(xb), G_x_static=Gd, out_kind=dq.OUT_NVFP4, G_out_static=G_o)
+        q_u = dq.dq_prefill_gemm(W, A=A, out_kind=dq.OUT_NVFP4, G_out_static=G_o)
+        if M:   # (M = 0: the minimum allocations hold no data)
+            assert torch.equal(q_f.codes, q_u.codes) and torch.equal(q_f.scales, q_u.scales)
+        assert torch.equal(q_f.G, q_u.G)
+
+
+def test_gemm_fused_c2_full_size_sampled():
+    """The 27B-class down projection with fused activation quantization
+    (M=8192, K=17408, N=5120) at full size; sampled rows and columns of the
+    bf16 output against the oracle (weights quantized with the whole
+    tensor's global scale)."""
+    cfg = synth.CONFIGS[2]
+    layer = cfg.layers[0]
+    w = synth.layer_weight(cfg, layer)
+    xb = synth.prefill_x(cfg, layer.k)
+    calib = synth.prefill_x(cfg, layer.k, calib=True)
+    G_x = nvfp4.global_scale(nvfp4.amax(formats.f32_from_bf16_bits(calib)))
+    W = dq.dq_pack_nvfp4(dev(w))
+    Y = dq.dq_prefill_gemm(W, X=bf16_dev(xb), G_x_static=dev(np.array([G_x], np.float32)), out_kind=dq.OUT_BF16)
+    rng = np.random.default_rng(73)
+    rows = np.sort(rng.choice(cfg.m, 16, replace=False))
+    cols = np.sort(rng.choice(layer.n, 512, replace=False))
+    qa, ca, _ = nvfp4.quantize_bf16_activations(xb[rows], G_x)
+    Gw = nvfp4.global_scale(nvfp4.amax(w))
+    qw, cw = nvfp4.quantize(w[cols], Gw)
+    ref = linalg.nvfp4_gemm(qa, ca, G_x, qw, cw, Gw)
+    y = host(Y[torch.from_numpy(rows).cuda()][:, torch.from_numpy(cols).cuda()].float()).astype(np.float64)
+    err = linalg.rel_fro(y, formats.bf16_rne_from_f64(ref))
+    say("  c2 fused sampled rel_fro", err)
+    assert err <= TOL
+
+
 def test_gemm_empty():
     W = dq.dq_pack_nvfp4(dev(synth.random_f32(1, (32, 64))))
     A = dq.dq_quantize_act_nvfp4(bf16_dev(np.zeros((0, 64), np.uint16)))
