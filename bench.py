@@ -12,18 +12,29 @@ One step = the whole per-token hot path over one batch:
   3. LUT3 decode GEMV at batch 1 and at batch 4 (fp32 y).
 Weight packing (NVFP4 and per-row LUT3) is offline and timed separately.
 
-The decode weights rotate over enough packed copies (>= 512 MiB) that every
-GEMV streams its weights from HBM rather than from the 256 MiB Infinity Cache;
-the activations X rotate over 16 copies for the same reason.
+The decode weights of a step rotate over enough packed copies (>= 768 MiB)
+that every GEMV streams its weights from HBM rather than from the 256 MiB
+Infinity Cache; the activations X rotate over 16 copies for the same reason.
+
+Besides the step, the run measures a decode sweep outside the timed steps:
+one decode token through 64 stacked 27B-class blocks (q/k/v 7168x5120,
+o 5120x5120, gate/up 34816x5120, down 5120x17408: 7.93 GB of LUT3 codes, all
+distinct memory) at batch 1, 8 and 16, and the same in LUT2 at batch 1.
 
 Prints one JSON line.  `value` is the prefill linear throughput: 2*M*N*K over
 (quantization + GEMM) time.  Per-kernel durations come from HIP events
 recorded on the launch stream around every kernel of the timed steps.
+
+`--calibrate-copy` instead runs a plain 256 MiB device copy five times: the
+reference kernel whose FETCH_SIZE / WRITE_SIZE readings scale the GEMM's
+counters into bytes (profiles/).
 """
 import argparse
 import ctypes
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -34,6 +45,9 @@ METRIC = "NVFP4 prefill GEMM TFLOPS (%FP4 peak); LUT3 decode GEMV GB/s (%HBM pea
 PEAK_FP16_TFLOPS = 2500.0      # dense fp16/bf16 MFMA, MI355X
 PEAK_FP4_TFLOPS = 10100.0      # dense fp4 MFMA, MI355X
 PEAK_HBM_GBS = 8000.0
+GEMM_SOURCE = os.path.join(ROOT, "paper_2609_26333_amd", "csrc", "gemm.hip")
+GEMM_COUNTERS = os.path.join(ROOT, "profiles", "nvfp4_gemm_8b_up_proj_counters.md")
+COPY_BYTES = 256 << 20
 
 
 def parse():
@@ -42,40 +56,129 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-decode-sweep", action="store_true")
+    p.add_argument("--sweep-blocks", type=int, default=64)
     p.add_argument("--decode-bytes", type=int, default=768 << 20,
                    help="total bytes of rotated decode weight copies")
+    p.add_argument("--calibrate-copy", action="store_true")
     return p.parse_args()
 
 
-def cpu_baseline(cfg, w, X, G_x, xd):
-    """Time the CPU oracle on a bounded sample of the same workload."""
-    import numpy as np
+def gemm_traffic():
+    """HBM bytes per GEMM launch from the committed counter summary: the
+    FETCH_SIZE and WRITE_SIZE readings of the GEMM, each scaled by the bytes
+    a plain copy of known size moves per KiB that the same counter reads.
+    None when the summary is missing or the GEMM source has changed since."""
+    try:
+        text = open(GEMM_COUNTERS).read()
+    except OSError:
+        return None
+    fields = dict(re.findall(r"^- `(\w+)`: `([^`]+)`", text, re.M))
+    sha = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
+    if fields.get("gemm_source_sha256") != sha:
+        return None
+    try:
+        fetch = float(fields["gemm_fetch_kib"]) * float(fields["fetch_bytes_per_kib"])
+        write = float(fields["gemm_write_kib"]) * float(fields["write_bytes_per_kib"])
+    except (KeyError, ValueError):
+        return None
+    return fetch + write
+
+
+def calibrate_copy():
+    import torch
+    torch.cuda.set_device(0)
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "device copy", "bytes_read": COPY_BYTES, "bytes_written": COPY_BYTES,
+                      "launches": 5}), flush=True)
+
+
+def cpu_baseline(cfg, w, X, G_x, xds, min_seconds=10.0):
+    """Time the CPU oracle on the same workload: the whole prefill layer
+    (activation quantization + fp64 GEMM over the dequantized operands) and
+    the batch-1 and batch-4 LUT3 GEMVs, repeated until min_seconds have
+    passed.  Weight packing is offline and untimed."""
     from threadpoolctl import threadpool_info
 
     from oracle import linalg, lut, nvfp4
-    N_s = 4096                                   # first third of the output features
-    w_s = w[:N_s]
-    qw, cw, Gw = nvfp4.quantize_dynamic(w_s)     # offline packing, not timed
-    codes, table = lut.quantize_per_row(w_s, 3)  # offline packing, not timed
-    t0 = time.perf_counter()
-    qa, ca, _ = nvfp4.quantize_bf16_activations(X, G_x)
-    Y = linalg.gemm(nvfp4.dequantize(qa, ca, G_x), nvfp4.dequantize(qw, cw, Gw))
-    t_pre = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    y = linalg.lut_gemv_per_row(xd, codes, table)
-    t_dec = time.perf_counter() - t0
+    qw, cw, Gw = nvfp4.quantize_dynamic(w)
+    codes, table = lut.quantize_per_row(w, 3)
+    w_hat = nvfp4.dequantize(qw, cw, Gw)
     M, K = X.shape
+    N = w.shape[0]
+    t_pre = t_dec = 0.0
+    reps = 0
+    start = time.perf_counter()
+    while reps == 0 or time.perf_counter() - start < min_seconds:
+        t0 = time.perf_counter()
+        qa, ca, _ = nvfp4.quantize_bf16_activations(X, G_x)
+        Y = linalg.gemm(nvfp4.dequantize(qa, ca, G_x), w_hat)
+        t1 = time.perf_counter()
+        for xd in xds.values():
+            linalg.lut_gemv_per_row(xd, codes, table)
+        t_pre += t1 - t0
+        t_dec += time.perf_counter() - t1
+        reps += 1
+        del Y
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    dec_bytes = N_s * K * 3 / 8 + N_s * 16 + xd.size * 2 + y.size * 4
-    del Y
+    dec_bytes = sum(N * K * 3 / 8 + N * 16 + xd.size * 2 + xd.shape[0] * N * 4 for xd in xds.values())
     return {
-        "value": 2.0 * M * N_s * K / t_pre / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-        "sample": (f"prefill: NVFP4 quantization of X[{M},{K}] + fp64 GEMM against the first {N_s} of "
-                   f"{w.shape[0]} weight rows ({t_pre:.2f} s); decode: LUT3 dequantization + fp64 GEMV "
-                   f"of those rows at batch 1 ({t_dec:.2f} s, {dec_bytes / t_dec / 1e9:.3f} GB/s); "
-                   f"weight packing untimed"),
-        "decode_gbps": dec_bytes / t_dec / 1e9,
+        "value": 2.0 * M * N * K * reps / t_pre / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+        "sample": (f"the whole layer {reps} times: NVFP4 quantization of X[{M},{K}] + fp64 GEMM against all "
+                   f"{N} weight rows ({t_pre / reps:.2f} s each); decode: LUT3 dequantization + fp64 GEMV at "
+                   f"batch {' and '.join(str(b) for b in xds)} ({t_dec / reps:.2f} s each, "
+                   f"{dec_bytes * reps / t_dec / 1e9:.3f} GB/s); weight packing untimed"),
+        "decode_gbps": dec_bytes * reps / t_dec / 1e9,
     }
+
+
+def decode_sweep(dq, synth, torch, np, n_blocks, steps):
+    """One decode token through n_blocks stacked 27B-class blocks (distinct
+    copies of one packed block), LUT3 at batch 1, 8, 16 and LUT2 at batch 1."""
+    cfg = synth.CONFIGS[4]
+    lib = dq.lib()
+    s = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(s.cuda_stream)
+    out = {}
+    Ws = [torch.from_numpy(synth.layer_weight(cfg, layer)).cuda() for layer in cfg.layers]
+    for bits, batches in ((3, (1, 8, 16)), (2, (1,))):
+        block = [dq.dq_pack_lut3(W, bits=bits, mode=dq.LUT_PER_ROW) for W in Ws]
+        if bits == 2:
+            del Ws
+        stack = [block] + [[dq.LutWeight(l.codes.clone(), l.lut.clone(), None, None, l.rows, l.cols, bits,
+                                         dq.LUT_PER_ROW) for l in block] for _ in range(n_blocks - 1)]
+        descs = [[l.desc() for l in blk] for blk in stack]
+        wbytes = sum(l.codes.numel() + l.lut.numel() * 2 for blk in stack for l in blk)
+        for B in batches:
+            xs = [torch.from_numpy(synth.decode_x(cfg, l.k, B).view(np.int16)).cuda() for l in cfg.layers]
+            ys = [torch.empty((B, l.n), dtype=torch.float32, device="cuda") for l in cfg.layers]
+            xp = [ctypes.c_void_p(t.data_ptr()) for t in xs]
+            yp = [ctypes.c_void_p(t.data_ptr()) for t in ys]
+
+            def token():
+                for d in descs:
+                    for i in range(len(cfg.layers)):
+                        assert lib.dq_decode_gemv(xp[i], B, ctypes.byref(d[i]), dq.OUT_F32, yp[i], sp) == 0
+            token()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            for _ in range(steps):
+                token()
+            e1.record(s)
+            torch.cuda.synchronize()
+            t = e0.elapsed_time(e1) / steps * 1e-3
+            io = n_blocks * sum(B * l.k * 2 + B * l.n * 4 for l in cfg.layers)
+            gbs = (wbytes + io) / t / 1e9
+            out[f"lut{bits}_b{B}"] = {"ms_per_token": t * 1e3, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
+                                      "weight_bytes": wbytes, "gemv_launches": n_blocks * len(cfg.layers)}
+        del stack, descs, block
+        torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -84,6 +187,9 @@ def main():
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
               f"(the sharded design is described in DESIGN.md)", file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     import numpy as np
     import torch
 
@@ -115,6 +221,7 @@ def main():
     e1.record()
     torch.cuda.synchronize()
     t_pack_lut = e0.elapsed_time(e1)
+    del W_dev
 
     # static activation scale from a calibration batch (running-max observer stand-in)
     A_cal = dq.dq_quantize_act_nvfp4(dev(calib.view(np.int16)))
@@ -194,6 +301,9 @@ def main():
         gbs = nbytes / (per[f"gemv_b{b}"] * 1e-3) / 1e9
         decode[f"b{b}"] = {"us": per[f"gemv_b{b}"] * 1e3, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
                            "bytes": nbytes}
+    # algorithmic bytes of one GEMM launch: the NVFP4 operands once, the bf16 output once
+    gemm_alg_bytes = M * K * (0.5 + 1 / 16) + N * K * (0.5 + 1 / 16) + M * N * 2
+    traffic = gemm_traffic()
 
     out = {
         "metric": METRIC, "value": prefill_tflops, "unit": "TFLOP/s", "n_gpus": 1,
@@ -213,12 +323,20 @@ def main():
         "pack_ms": {"nvfp4": t_pack_nvfp4, "lut3_per_row": t_pack_lut},
         "roofline": {"bound": "mfma", "kernel": "nvfp4_gemm_kernel", "achieved": gemm_tflops,
                      "peak": PEAK_FP16_TFLOPS, "unit": "TFLOP/s", "frac": gemm_tflops / PEAK_FP16_TFLOPS,
-                     "traffic": None,
+                     "traffic": traffic,
+                     "traffic_note": (f"HBM bytes per GEMM launch from FETCH_SIZE + WRITE_SIZE (copy-calibrated); "
+                                      f"algorithmic bytes {gemm_alg_bytes:.4g}" if traffic is not None else
+                                      "no counter summary for the current GEMM source"),
                      "note": "exact NVFP4 operands are dequantized to fp16 and multiplied on fp16 MFMA; "
                              "frac of the dense FP4 peak is prefill.frac_fp4_peak"},
     }
+    del Wls, dWls, Xs
+    torch.cuda.empty_cache()
+    if not args.no_decode_sweep:
+        out["decode_sweep_27b_blocks"] = decode_sweep(dq, synth, torch, np, args.sweep_blocks, 5)
+        out["decode_sweep_27b_blocks"]["blocks"] = args.sweep_blocks
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, w, X, np.float32(G_x_host), xds[1])
+        out["cpu_baseline"] = cpu_baseline(cfg, w, X, np.float32(G_x_host), xds)
     print(json.dumps(out), flush=True)
 
 
