@@ -92,13 +92,23 @@ def test_gemv_paper_grid_rational():
 
 
 def test_silu_mul_values():
-    g = np.array([0.0, 1.0, -2.0, 30.0])
-    u = np.array([5.0, 2.0, 1.0, 1.0])
+    """SwiGLU's silu(g) * u pinned by facts independent of the oracle's
+    formula: other closed forms of the logistic function (the tanh form
+    (1 + tanh(g/2)) / 2 for g >= 0, e^g / (1 + e^g) for g < 0, each free of
+    cancellation on its side), the identity silu(g) - silu(-g) = g,
+    silu(0) = 0, and the limits silu(g) -> g (g -> +inf) and -> 0 (g -> -inf)."""
+    rng = np.random.default_rng(5)
+    g = rng.standard_normal(1000) * 4
+    u = rng.standard_normal(1000)
+    sig = np.where(g >= 0, (1.0 + np.tanh(g / 2.0)) / 2.0, np.exp(np.minimum(g, 0)) / (1.0 + np.exp(np.minimum(g, 0))))
+    other = g * sig * u
     out = linalg.silu_mul(g, u)
-    assert out[0] == 0.0
-    assert abs(out[1] - 2.0 / (1 + np.exp(-1.0))) < 1e-15
-    assert abs(out[2] + 2.0 / (1 + np.exp(2.0))) < 1e-15
-    assert abs(out[3] - 30.0) < 1e-9
+    assert np.max(np.abs(out - other) / np.maximum(np.abs(other), 1e-300)) < 1e-13
+    ones = np.ones_like(g)
+    assert np.allclose(linalg.silu_mul(g, ones) - linalg.silu_mul(-g, ones), g, rtol=0, atol=1e-13)
+    assert linalg.silu_mul(np.array([0.0]), np.array([7.0]))[0] == 0.0
+    big = linalg.silu_mul(np.array([60.0, -60.0]), np.array([1.0, 1.0]))
+    assert big[0] == 60.0 and 0 > big[1] > -1e-20
 
 
 def test_rel_fro():
