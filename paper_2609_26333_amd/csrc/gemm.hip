@@ -13,15 +13,18 @@
 // global scales are applied once in the epilogue.
 //
 // Structure
-//  * a workgroup of 2 x WN wavefronts covers a 256 x (32*NBW*WN) output tile;
-//    each wavefront owns 128 x 32*NBW (4 x NBW accumulator blocks of 32x32),
-//    two wavefronts per SIMD;
+//  * a workgroup of WM x WN wavefronts covers a (32*TM*WM) x (32*TN*WN)
+//    output tile; each wavefront owns 32*TM x 32*TN (TM x TN accumulator
+//    blocks of 32x32).  The default is four wavefronts of 128 x 128 on a
+//    256 x 256 tile, one wavefront per SIMD: each operand tile is dequantized
+//    by two wavefronts (not four), and 64 MFMAs per K step give the
+//    dequantization of the next sub-step room to run between them;
 //  * operands stay compressed (4.5 bits/element) until they reach registers:
-//    a ring of kStages LDS stages, each holding the raw code and scale tiles
-//    of KS 64-column K steps, is filled by direct global->LDS loads
-//    (global_load_lds_dwordx4 / _dword) kStages-1 stages ahead, so the HBM
-//    and L2 latency is hidden without spending VGPRs on prefetch; one
-//    workgroup barrier per stage;
+//    a ring of LDS stages, each holding the raw code and scale tiles of KS
+//    64-column K steps, is filled by direct global->LDS loads
+//    (global_load_lds_dwordx4 / _dword) stages-1 ahead, so the HBM and L2
+//    latency is hidden without spending VGPRs on prefetch; one workgroup
+//    barrier per stage;
 //  * within a stage, a 32x64 code tile is one contiguous KiB; the loading
 //    lane i fetches 16-byte chunk 2*(i%32) + i/32 so that the consuming lane
 //    l (row l%32, columns 32*(l/32)..+31) reads LDS bytes 16l..16l+15
@@ -30,6 +33,8 @@
 //    operands (a permutation of K shared by A and W);
 //  * workgroups are numbered so that the 8 XCDs each own a contiguous range
 //    of output-column panels (W panels stay in one XCD's L2).
+#include <type_traits>
+
 #include "dq_device.hpp"
 #include "dq_internal.hpp"
 
@@ -37,30 +42,40 @@ namespace dq {
 
 namespace {
 
-constexpr int kBlkM = 256;
 constexpr int kLdsBudget = 150 * 1024;   // of gfx950's 160 KiB
 
-// Workgroup geometry: WN wavefront columns x 2 wavefront rows; a wavefront
-// owns 128 rows x 32*NBW columns, so the workgroup tile is 256 x 32*NBW*WN.
-template <int WN, int NBW, int KS>
+// Workgroup geometry: WM x WN wavefronts, each owning 32*TM rows x 32*TN
+// columns; KS 64-column K steps per LDS stage.
+template <int TM, int TN, int WM, int WN, int KS>
 struct Geo {
-  static constexpr int waves = 2 * WN;
+  static constexpr int tm = TM, tn = TN, wm = WM, wn = WN;
+  static constexpr int waves = WM * WN;
   static constexpr int threads = 64 * waves;
-  static constexpr int bn = 32 * NBW * WN;     // workgroup tile columns
+  static constexpr int bm = 32 * TM * WM;      // workgroup tile rows
+  static constexpr int bn = 32 * TN * WN;      // workgroup tile columns
+  static constexpr int at = bm / 32;           // A code tiles per K step
   static constexpr int wt = bn / 32;           // W code tiles per K step
   static constexpr int ks = KS;                // 64-column K steps per stage (one barrier each)
-  // LDS byte layout of one stage, per K step u: A codes (8 KiB), W codes,
-  // A scales (1 KiB), W scales
-  static constexpr int step_bytes = 8 * 1024 + wt * 1024 + 8 * 128 + wt * 128;
+  // LDS byte layout of one stage, per K step u: A codes, W codes, A scales, W scales
+  static constexpr int step_bytes = at * 1024 + wt * 1024 + at * 128 + wt * 128;
   static constexpr int a_codes = 0;
-  static constexpr int w_codes = 8 * 1024;
+  static constexpr int w_codes = at * 1024;
   static constexpr int a_scales = w_codes + wt * 1024;
-  static constexpr int w_scales = a_scales + 8 * 128;
+  static constexpr int w_scales = a_scales + at * 128;
   static constexpr int bytes = KS * step_bytes;
-  static constexpr int stages = kLdsBudget / bytes;   // ring depth
-  // direct-to-LDS instructions per K step: 8 + wt code tiles, (8 + wt) / 2 scale pairs
-  static constexpr int code_loads = 8 + wt;
-  static constexpr int scale_loads = (8 + wt) / 2;
+  // fp16 copy of the workgroup's A tiles for one K step (dequantized once,
+  // read by every wavefront of the row); double-buffered after the ring
+  static constexpr int a16_tile = 32 * 64 * 2;
+  static constexpr int a16_bytes = at * a16_tile;
+  static constexpr int stages = (kLdsBudget - 2 * a16_bytes) / bytes;   // ring depth
+  static constexpr int a16_base = stages * bytes;
+  // direct-to-LDS instructions per K step: one per code tile, one per pair of scale tiles
+  static constexpr int code_loads = at + wt;
+  static constexpr int scale_loads = (at + wt) / 2;
+  static_assert(at % 2 == 0 && wt % 2 == 0, "scale tiles are loaded in pairs");
+  static_assert(stages >= 3, "LDS ring needs three stages");
+  static_assert(waves == at, "each wavefront dequantizes one A tile per K step");
+  static_assert(KS == 1, "one K step per stage");
 };
 
 // 8 E2M1 codes (one dword) times an fp16 block scale -> 8 exact fp16 values.
@@ -101,8 +116,8 @@ __device__ inline void issue_stage(uint8_t* stage, const uint8_t* __restrict__ a
   for (int u = 0; u < Gm::ks; ++u, ++kt, stage += Gm::step_bytes) {
   const int64_t ktc = kt < KT ? kt : KT - 1;             // past the end of K: reload the last step
   for (int t = wave; t < Gm::code_loads; t += Gm::waves) {
-    const bool is_a = t < 8;
-    const int b = is_a ? t : t - 8;
+    const bool is_a = t < Gm::at;
+    const int b = is_a ? t : t - Gm::at;
     const int64_t lim = is_a ? a_tiles_r : w_tiles_r;
     int64_t tr = (is_a ? a_tr0 : w_tr0) + b;
     tr = tr < lim ? tr : lim - 1;
@@ -111,8 +126,8 @@ __device__ inline void issue_stage(uint8_t* stage, const uint8_t* __restrict__ a
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src), reinterpret_cast<void*>(dst), 16, 0, 0);
   }
   for (int t = wave; t < Gm::scale_loads; t += Gm::waves) {
-    const bool is_a = t < 4;
-    const int b = 2 * (is_a ? t : t - 4) + (lane >> 5);
+    const bool is_a = t < Gm::at / 2;
+    const int b = 2 * (is_a ? t : t - Gm::at / 2) + (lane >> 5);
     const int64_t lim = is_a ? a_tiles_r : w_tiles_r;
     int64_t tr = (is_a ? a_tr0 : w_tr0) + b;
     tr = tr < lim ? tr : lim - 1;
@@ -128,17 +143,6 @@ __device__ inline void issue_stage(uint8_t* stage, const uint8_t* __restrict__ a
 template <int n>
 __device__ inline void wait_vm() {
   __builtin_amdgcn_s_waitcnt((n & 0xF) | (0x7 << 4) | (0xF << 8) | ((n >> 4) << 14));
-}
-__device__ inline void wait_vm_dyn(int n) {
-  switch (n) {
-#define DQ_VM(k) case k: wait_vm<k>(); break;
-    DQ_VM(0) DQ_VM(1) DQ_VM(2) DQ_VM(3) DQ_VM(4) DQ_VM(5) DQ_VM(6) DQ_VM(7) DQ_VM(8) DQ_VM(9)
-    DQ_VM(10) DQ_VM(11) DQ_VM(12) DQ_VM(13) DQ_VM(14) DQ_VM(15) DQ_VM(16) DQ_VM(17) DQ_VM(18)
-    DQ_VM(19) DQ_VM(20) DQ_VM(21) DQ_VM(22) DQ_VM(23) DQ_VM(24) DQ_VM(25) DQ_VM(26) DQ_VM(27)
-    DQ_VM(28) DQ_VM(29) DQ_VM(30) DQ_VM(31)
-#undef DQ_VM
-    default: wait_vm<0>(); break;
-  }
 }
 
 // Workgroup barrier without the release/acquire fences of __syncthreads (which
@@ -175,14 +179,14 @@ __device__ inline uint32_t e2m1_code(float v, float S) {
   return fp4_canonical_zero(cvt_pk_fp4<0>(0u, div_by_scale(v, S, rcp), 0.0f)) & 0xFu;
 }
 
-template <int WN, int NBW, int KS, int OUT, bool SW>
-__global__ __launch_bounds__(64 * 2 * WN, 1) void nvfp4_gemm_kernel(
+template <class Gm, int OUT, bool SW>
+__global__ __launch_bounds__(Gm::threads, 1) void nvfp4_gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales, const float* __restrict__ Ga,
     const uint8_t* __restrict__ w_codes, const uint8_t* __restrict__ w_scales, const float* __restrict__ Gw,
     int64_t M, int64_t N, int64_t a_tiles_r, int64_t w_tiles_r, int64_t KT, GemmOut out,
     int64_t tiles_m, int64_t tiles_n) {
-  typedef Geo<WN, NBW, KS> Gm;
   constexpr int kStages = Gm::stages;
+  constexpr int TM = Gm::tm, TN = Gm::tn, KS = Gm::ks;
   extern __shared__ __align__(16) uint8_t smem[];
 
   const int lane = threadIdx.x & 63;
@@ -195,91 +199,157 @@ __global__ __launch_bounds__(64 * 2 * WN, 1) void nvfp4_gemm_kernel(
   int64_t logical = blockIdx.x;
   if (nb % 8 == 0) logical = (int64_t)(blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8;
   const int64_t bm = logical % tiles_m, bn = logical / tiles_m;
-  const int wm = wave & 1, wn = wave >> 1;
-  const int64_t a_tr0 = bm * (kBlkM / 32), w_tr0 = bn * Gm::wt;
-  const int64_t m0 = bm * kBlkM + wm * 128;
-  const int64_t n0 = bn * Gm::bn + wn * 32 * NBW;
+  const int wm = wave % Gm::wm, wn = wave / Gm::wm;
+  const int64_t a_tr0 = bm * Gm::at, w_tr0 = bn * Gm::wt;
+  const int64_t m0 = bm * Gm::bm + wm * 32 * TM;
+  const int64_t n0 = bn * Gm::bn + wn * 32 * TN;
 
-  float16_t acc[4][NBW];
+  float16_t acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < NBW; ++j) acc[i][j] = float16_t{};
+    for (int j = 0; j < TN; ++j) acc[i][j] = float16_t{};
 
-  const int64_t NST = (KT + KS - 1) / KS;     // stages of KS K steps
-  // prologue: stages 0 .. kStages-2
+  constexpr int S = kStages;
+  const int KTi = (int)KT;
+  static_assert(Gm::at == Gm::waves && Gm::wt == Gm::waves, "one A and one W code tile per wavefront and stage");
+  static_assert(Gm::scale_loads == Gm::waves, "one scale-pair load per wavefront and stage");
+
+  // Direct loads of one stage (= K step): this wavefront fetches A code tile
+  // `wave`, W code tile `wave` and one pair of scale tiles (A pairs for the
+  // first half of the wavefronts, W pairs for the second).  Rows past the end
+  // of an operand read the last row tile (in bounds; zeroed on use).
+  const int chunk = 2 * (lane & 31) + (lane >> 5);      // 16-byte chunk of the tile fetched by this lane
+  const uint8_t* a_src = a_codes + (min(a_tr0 + wave, a_tiles_r - 1) * KT) * 1024 + chunk * 16;
+  const uint8_t* w_src = w_codes + (min(w_tr0 + wave, w_tiles_r - 1) * KT) * 1024 + chunk * 16;
+  constexpr int half_waves = Gm::waves / 2;
+  const bool s_is_a = wave < half_waves;
+  const int s_pair = s_is_a ? wave : wave - half_waves;
+  const int64_t s_tr = min((s_is_a ? a_tr0 : w_tr0) + 2 * s_pair + (lane >> 5), (s_is_a ? a_tiles_r : w_tiles_r) - 1);
+  const uint8_t* s_src = (s_is_a ? a_scales : w_scales) + (s_tr * KT) * 128 + (lane & 31) * 4;
+  const int s_dst = (s_is_a ? Gm::a_scales : Gm::w_scales) + 2 * s_pair * 128;
+  auto issue = [&](int kt) {
+    uint8_t* stage = smem + (kt % S) * Gm::bytes;
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(a_src + (size_t)kt * 1024),
+                                     reinterpret_cast<void*>(stage + Gm::a_codes + wave * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(w_src + (size_t)kt * 1024),
+                                     reinterpret_cast<void*>(stage + Gm::w_codes + wave * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(s_src + (size_t)kt * 128),
+                                     reinterpret_cast<void*>(stage + s_dst), 4, 0, 0);
+  };
+  constexpr int L = 3;   // direct loads per wavefront and stage
+  // prologue: stages (= K steps) 0 .. S-1
 #pragma unroll
-  for (int st = 0; st < kStages - 1; ++st)
-    if (st < NST)
-      issue_stage<Gm>(smem + st * Gm::bytes, a_codes, a_scales, w_codes, w_scales, a_tr0, a_tiles_r, w_tr0,
-                      w_tiles_r, (int64_t)st * KS, KT, wave, lane);
-  const int L = loads_per_stage<Gm>(wave);
+  for (int st = 0; st < S; ++st)
+    if (st < KTi) issue(st);
+  // this wavefront's loads of stage `need` have landed, given stages up to
+  // `last` issued (the later ones, at most S - 2, may stay in flight)
+  auto wait_stage = [&](int need, int last) {
+    const int ahead = max(0, min(last, KTi - 1) - need);
+    if (ahead >= 2) wait_vm<2 * L>();
+    else if (ahead == 1) wait_vm<L>();
+    else wait_vm<0>();
+  };
+  static_assert(S - 2 <= 2, "wait_stage covers at most two stages in flight");
 
   // rows / columns of this wavefront that exist (zero inputs elsewhere)
-  bool a_ok[4], w_ok[NBW];
+  bool w_ok[TN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) a_ok[i] = (m0 / 32 + i) < a_tiles_r;
-#pragma unroll
-  for (int j = 0; j < NBW; ++j) w_ok[j] = (n0 / 32 + j) < w_tiles_r;
+  for (int j = 0; j < TN; ++j) w_ok[j] = (n0 / 32 + j) < w_tiles_r;
   const int lane_scale = (lane & 31) * 4 + (lane >> 5) * 2;
-
-  for (int64_t st = 0; st < NST; ++st) {
-    // wait until this wavefront's loads of stage st have landed (the loads of
-    // the stages issued after it may stay in flight), then for all wavefronts
-    const int ahead = (int)min((int64_t)kStages - 2, NST - 1 - st);
-    wait_vm_dyn(ahead * L);
-    lds_barrier();
-    // refill the stage consumed in the previous iteration
-    if (st + kStages - 1 < NST)
-      issue_stage<Gm>(smem + ((st + kStages - 1) % kStages) * Gm::bytes, a_codes, a_scales, w_codes, w_scales,
-                      a_tr0, a_tiles_r, w_tr0, w_tiles_r, (st + kStages - 1) * KS, KT, wave, lane);
-
+  const int row = lane & 31, half = lane >> 5;
+  // Swizzle of the fp16 A tiles: 16-byte chunk c of row r is stored at chunk
+  // c ^ g(r), g(r) = (r % 8) ^ (r / 8 % 2), so that any 8 or 16 consecutive
+  // lanes of the producer's writes and of the MFMA operand reads touch
+  // distinct banks (for 32 or 64 four-byte banks).
+  const int gsw = (row & 7) ^ ((row >> 3) & 1);
+  int a_rd[4], a_wr[4];   // per-lane byte offsets of the read / written chunks
 #pragma unroll
-    for (int u = 0; u < KS; ++u) {
-      if (st * KS + u >= KT) break;                    // a partial last stage
-      const uint8_t* stg = smem + (st % kStages) * Gm::bytes + u * Gm::step_bytes;
-      uint4_t ac[4], wc[NBW];
-      uint32_t asc[4], wsc[NBW];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int b = wm * 4 + i;
-        ac[i] = *reinterpret_cast<const uint4_t*>(stg + Gm::a_codes + b * 1024 + lane * 16);
-        asc[i] = *reinterpret_cast<const uint16_t*>(stg + Gm::a_scales + b * 128 + lane_scale);
-        if (!a_ok[i]) {
-          ac[i] = uint4_t{0u, 0u, 0u, 0u};
-          asc[i] = 0u;
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < NBW; ++j) {
-        const int b = wn * NBW + j;
-        wc[j] = *reinterpret_cast<const uint4_t*>(stg + Gm::w_codes + b * 1024 + lane * 16);
-        wsc[j] = *reinterpret_cast<const uint16_t*>(stg + Gm::w_scales + b * 128 + lane_scale);
-        if (!w_ok[j]) {
-          wc[j] = uint4_t{0u, 0u, 0u, 0u};
-          wsc[j] = 0u;
-        }
-      }
-      half2_t as_[4][2], ws_[NBW][2];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) scale_pairs(asc[i], as_[i][0], as_[i][1]);
-#pragma unroll
-      for (int j = 0; j < NBW; ++j) scale_pairs(wsc[j], ws_[j][0], ws_[j][1]);
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        half8_t af[4], wf[NBW];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) af[i] = dequant8(ac[i][s], as_[i][s >> 1]);
-#pragma unroll
-        for (int j = 0; j < NBW; ++j) wf[j] = dequant8(wc[j][s], ws_[j][s >> 1]);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < NBW; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], wf[j], acc[i][j], 0, 0, 0);
-      }
-    }
+  for (int k = 0; k < 4; ++k) {
+    a_rd[k] = Gm::a16_base + wm * TM * Gm::a16_tile + row * 128 + (((4 * half + k) ^ gsw) * 16);
+    a_wr[k] = Gm::a16_base + wave * Gm::a16_tile + row * 128 + (((4 * half + k) ^ gsw) * 16);
   }
+  const int w_rd = Gm::w_codes + wn * TN * 1024 + lane * 16;
+  const int ws_rd = Gm::w_scales + wn * TN * 128 + lane_scale;
+  const int a_prd = Gm::a_codes + wave * 1024 + lane * 16;
+  const int as_prd = Gm::a_scales + wave * 128 + lane_scale;
+
+  // Producer: A tile `wave` of K step kt, dequantized to fp16 into buffer BUF.
+  const bool p_ok = (a_tr0 + wave) < a_tiles_r;
+  auto produce = [&](int kt, auto buf) {
+    const uint8_t* stg = smem + (kt % S) * Gm::bytes;
+    const uint4_t c = *reinterpret_cast<const uint4_t*>(stg + a_prd);
+    uint32_t sc = *reinterpret_cast<const uint16_t*>(stg + as_prd);
+    if (!p_ok) sc = 0u;   // a zero scale zeroes the (finite) codes of a missing tile
+    half2_t s_lo, s_hi;
+    scale_pairs(sc, s_lo, s_hi);
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      *reinterpret_cast<half8_t*>(smem + a_wr[k] + decltype(buf)::value * Gm::a16_bytes) =
+          dequant8(c[k], k < 2 ? s_lo : s_hi);
+  };
+  auto lgkm0 = [] {
+    __builtin_amdgcn_s_waitcnt((0x3F & 0xF) | (0x7 << 4) | (0x0 << 8) | ((0x3F >> 4) << 14));   // lgkmcnt(0)
+  };
+  // One K step on A buffer BUF: produce the next step's A into the other
+  // buffer, dequantize this wavefront's W tiles, run the MFMAs; then the
+  // step's barrier (A of step kt+1 written, stage kt+2 landed, stage kt's slot
+  // and buffer BUF free) and the refill of stage kt's slot.
+  auto step = [&](int kt, auto buf) {
+    using other = std::integral_constant<int, 1 - decltype(buf)::value>;
+    if (kt + 1 < KTi) produce(kt + 1, other{});
+    const uint8_t* stg = smem + (kt % S) * Gm::bytes;
+    uint4_t wc[TN];
+    half2_t ws_[TN][2];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      wc[j] = *reinterpret_cast<const uint4_t*>(stg + w_rd + j * 1024);
+      uint32_t wsc = *reinterpret_cast<const uint16_t*>(stg + ws_rd + j * 128);
+      if (!w_ok[j]) wsc = 0u;
+      scale_pairs(wsc, ws_[j][0], ws_[j][1]);
+    }
+    auto a_frag = [&](int i, int s) -> half8_t {
+      return *reinterpret_cast<const half8_t*>(smem + a_rd[s] + decltype(buf)::value * Gm::a16_bytes +
+                                               i * Gm::a16_tile);
+    };
+    // sub-step s+1's operands (A from LDS, W dequantized) are prepared while
+    // sub-step s's MFMAs run
+    half8_t af[2][TM], wf[2][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) af[0][i] = a_frag(i, 0);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) wf[0][j] = dequant8(wc[j][0], ws_[j][0]);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s < 3) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) af[(s + 1) & 1][i] = a_frag(i, s + 1);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) wf[(s + 1) & 1][j] = dequant8(wc[j][s + 1], ws_[j][(s + 1) >> 1]);
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[s & 1][i], wf[s & 1][j], acc[i][j], 0, 0, 0);
+    }
+    lgkm0();
+    if (kt + 2 < KTi) wait_stage(kt + 2, kt + S - 1);
+    lds_barrier();
+    if (kt + S < KTi) issue(kt + S);
+  };
+
+  wait_stage(KTi > 1 ? 1 : 0, S - 1);
+  lds_barrier();
+  produce(0, std::integral_constant<int, 0>{});
+  lgkm0();
+  lds_barrier();
+  int kt = 0;
+  for (; kt + 1 < KTi; kt += 2) {   // A buffers alternate: 0 on even steps, 1 on odd steps
+    step(kt, std::integral_constant<int, 0>{});
+    step(kt + 1, std::integral_constant<int, 1>{});
+  }
+  if (kt < KTi) step(kt, std::integral_constant<int, 0>{});
 
   const float g = (*Ga) * (*Gw);
   const int col_in = lane & 31;
@@ -291,9 +361,9 @@ __global__ __launch_bounds__(64 * 2 * WN, 1) void nvfp4_gemm_kernel(
   // (n0 + 32j) / 2 + col_in.
   if constexpr (OUT != kOutNvfp4) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < TM; ++i) {
 #pragma unroll
-      for (int j = 0; j < NBW; ++j) {
+      for (int j = 0; j < TN; ++j) {
         const int64_t gcol = n0 + j * 32 + col_in;
         const int64_t col = SW ? (n0 + j * 32) / 2 + col_in : gcol;
         const bool col_ok = SW ? (col_in < 16 && col < out.Nout) : gcol < N;
@@ -319,11 +389,11 @@ __global__ __launch_bounds__(64 * 2 * WN, 1) void nvfp4_gemm_kernel(
     const float den = 6.0f * Go;
     if (blockIdx.x == 0 && threadIdx.x == 0 && out.G != out.G_out) *out.G = Go;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < TM; ++i) {
       const int64_t tr = (m0 + i * 32) / 32;
       if (tr >= out.tiles_r) continue;
 #pragma unroll
-      for (int j = 0; j < NBW; ++j) {
+      for (int j = 0; j < TN; ++j) {
         const int64_t gcol = n0 + j * 32 + col_in;
         const int64_t cbase = SW ? (n0 + j * 32) / 2 : n0 + j * 32;   // first output column of the block
         const int64_t tc = cbase / 64;
@@ -360,14 +430,14 @@ __global__ __launch_bounds__(64 * 2 * WN, 1) void nvfp4_gemm_kernel(
   }
 }
 
-template <int WN, int NBW, int KS>
+template <class Gm>
 hipError_t launch_geo(const GemmArgs& a, hipStream_t s) {
-  typedef Geo<WN, NBW, KS> Gm;
   const int64_t a_tiles_r = round_up(a.M, 32) / 32;
   const int64_t w_tiles_r = round_up(a.N, 32) / 32;
   const int64_t KT = round_up(a.K, 64) / 64;
-  const int64_t tiles_m = (a.M + kBlkM - 1) / kBlkM, tiles_n = (a.N + Gm::bn - 1) / Gm::bn;
-  const size_t lds = (size_t)Gm::stages * Gm::bytes;
+  const int64_t tiles_m = (a.M + Gm::bm - 1) / Gm::bm, tiles_n = (a.N + Gm::bn - 1) / Gm::bn;
+  const size_t lds = (size_t)Gm::a16_base + 2 * (size_t)Gm::a16_bytes;   // fp4 ring + fp16 A buffers
+  static_assert(Gm::a16_base + 2 * Gm::a16_bytes <= kLdsBudget, "LDS budget");
   const bool sw = (a.flags & 1) != 0;
   GemmOut o{};
   o.Y = a.Y;
@@ -383,9 +453,9 @@ hipError_t launch_geo(const GemmArgs& a, hipStream_t s) {
   typedef void (*kern_t)(const uint8_t*, const uint8_t*, const float*, const uint8_t*, const uint8_t*, const float*,
                          int64_t, int64_t, int64_t, int64_t, int64_t, GemmOut, int64_t, int64_t);
   static const kern_t kerns[3][2] = {
-      {nvfp4_gemm_kernel<WN, NBW, KS, kOutF32, false>, nvfp4_gemm_kernel<WN, NBW, KS, kOutF32, true>},
-      {nvfp4_gemm_kernel<WN, NBW, KS, kOutBF16, false>, nvfp4_gemm_kernel<WN, NBW, KS, kOutBF16, true>},
-      {nvfp4_gemm_kernel<WN, NBW, KS, kOutNvfp4, false>, nvfp4_gemm_kernel<WN, NBW, KS, kOutNvfp4, true>}};
+      {nvfp4_gemm_kernel<Gm, kOutF32, false>, nvfp4_gemm_kernel<Gm, kOutF32, true>},
+      {nvfp4_gemm_kernel<Gm, kOutBF16, false>, nvfp4_gemm_kernel<Gm, kOutBF16, true>},
+      {nvfp4_gemm_kernel<Gm, kOutNvfp4, false>, nvfp4_gemm_kernel<Gm, kOutNvfp4, true>}};
   const kern_t kern = kerns[a.out_kind][sw ? 1 : 0];
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
@@ -406,9 +476,8 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(publish_scale_kernel, dim3(1), dim3(1), 0, s, a.G_out, a.Yq.G);
     return hipGetLastError();
   }
-  // 256x256 workgroup tiles as 2x4 wavefronts of 128x64 (two wavefronts per
-  // SIMD hide each other's LDS / barrier / load stalls).
-  return launch_geo<4, 2, 2>(a, s);
+  // 256x256 workgroup tiles as 2x4 wavefronts of 128x64, two per SIMD
+  return launch_geo<Geo<4, 2, 2, 4, 1>>(a, s);
 }
 
 }  // namespace dq
