@@ -67,7 +67,8 @@ struct Geo {
   // read by every wavefront of the row); double-buffered after the ring
   static constexpr int a16_tile = 32 * 64 * 2;
   static constexpr int a16_bytes = at * a16_tile;
-  static constexpr int stages = (kLdsBudget - 2 * a16_bytes) / bytes;   // ring depth
+  static constexpr int stages_fit = (kLdsBudget - 2 * a16_bytes) / bytes;
+  static constexpr int stages = stages_fit < 4 ? stages_fit : 4;   // ring depth
   static constexpr int a16_base = stages * bytes;
   // direct-to-LDS instructions per K step: one per code tile, one per pair of scale tiles
   static constexpr int code_loads = at + wt;
@@ -75,6 +76,7 @@ struct Geo {
   static_assert(at % 2 == 0 && wt % 2 == 0, "scale tiles are loaded in pairs");
   static_assert(stages >= 3, "LDS ring needs three stages");
   static_assert(waves == at, "each wavefront dequantizes one A tile per K step");
+  static_assert(wt <= waves && (at + wt) / 2 <= waves, "at most one W tile and one scale pair per wavefront");
   static_assert(KS == 1, "one K step per stage");
 };
 
@@ -184,7 +186,7 @@ __global__ __launch_bounds__(Gm::threads, 1) void nvfp4_gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales, const float* __restrict__ Ga,
     const uint8_t* __restrict__ w_codes, const uint8_t* __restrict__ w_scales, const float* __restrict__ Gw,
     int64_t M, int64_t N, int64_t a_tiles_r, int64_t w_tiles_r, int64_t KT, GemmOut out,
-    int64_t tiles_m, int64_t tiles_n) {
+    int64_t tiles_m, int64_t tiles_n, int64_t n_off) {
   constexpr int kStages = Gm::stages;
   constexpr int TM = Gm::tm, TN = Gm::tn, KS = Gm::ks;
   extern __shared__ __align__(16) uint8_t smem[];
@@ -200,9 +202,10 @@ __global__ __launch_bounds__(Gm::threads, 1) void nvfp4_gemm_kernel(
   if (nb % 8 == 0) logical = (int64_t)(blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8;
   const int64_t bm = logical % tiles_m, bn = logical / tiles_m;
   const int wm = wave % Gm::wm, wn = wave / Gm::wm;
-  const int64_t a_tr0 = bm * Gm::at, w_tr0 = bn * Gm::wt;
+  // this launch covers tiles_n column panels from output column n_off on
+  const int64_t a_tr0 = bm * Gm::at, w_tr0 = n_off / 32 + bn * Gm::wt;
   const int64_t m0 = bm * Gm::bm + wm * 32 * TM;
-  const int64_t n0 = bn * Gm::bn + wn * 32 * TN;
+  const int64_t n0 = n_off + bn * Gm::bn + wn * 32 * TN;
 
   float16_t acc[TM][TN];
 #pragma unroll
@@ -212,19 +215,19 @@ __global__ __launch_bounds__(Gm::threads, 1) void nvfp4_gemm_kernel(
 
   constexpr int S = kStages;
   const int KTi = (int)KT;
-  static_assert(Gm::at == Gm::waves && Gm::wt == Gm::waves, "one A and one W code tile per wavefront and stage");
-  static_assert(Gm::scale_loads == Gm::waves, "one scale-pair load per wavefront and stage");
-
   // Direct loads of one stage (= K step): this wavefront fetches A code tile
-  // `wave`, W code tile `wave` and one pair of scale tiles (A pairs for the
-  // first half of the wavefronts, W pairs for the second).  Rows past the end
-  // of an operand read the last row tile (in bounds; zeroed on use).
+  // `wave`, W code tile `wave` (if there is one) and one pair of scale tiles
+  // (A pairs first, then W pairs, one per wavefront while they last).  Rows
+  // past the end of an operand read the last row tile (in bounds; zeroed on
+  // use).
   const int chunk = 2 * (lane & 31) + (lane >> 5);      // 16-byte chunk of the tile fetched by this lane
   const uint8_t* a_src = a_codes + (min(a_tr0 + wave, a_tiles_r - 1) * KT) * 1024 + chunk * 16;
-  const uint8_t* w_src = w_codes + (min(w_tr0 + wave, w_tiles_r - 1) * KT) * 1024 + chunk * 16;
-  constexpr int half_waves = Gm::waves / 2;
-  const bool s_is_a = wave < half_waves;
-  const int s_pair = s_is_a ? wave : wave - half_waves;
+  const bool has_w = wave < Gm::wt;
+  const uint8_t* w_src = w_codes + (min(w_tr0 + (has_w ? wave : 0), w_tiles_r - 1) * KT) * 1024 + chunk * 16;
+  constexpr int a_pairs = Gm::at / 2, pairs = (Gm::at + Gm::wt) / 2;
+  const bool has_s = wave < pairs;
+  const bool s_is_a = wave < a_pairs;
+  const int s_pair = !has_s ? 0 : s_is_a ? wave : wave - a_pairs;
   const int64_t s_tr = min((s_is_a ? a_tr0 : w_tr0) + 2 * s_pair + (lane >> 5), (s_is_a ? a_tiles_r : w_tiles_r) - 1);
   const uint8_t* s_src = (s_is_a ? a_scales : w_scales) + (s_tr * KT) * 128 + (lane & 31) * 4;
   const int s_dst = (s_is_a ? Gm::a_scales : Gm::w_scales) + 2 * s_pair * 128;
@@ -232,12 +235,17 @@ __global__ __launch_bounds__(Gm::threads, 1) void nvfp4_gemm_kernel(
     uint8_t* stage = smem + (kt % S) * Gm::bytes;
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(a_src + (size_t)kt * 1024),
                                      reinterpret_cast<void*>(stage + Gm::a_codes + wave * 1024), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(w_src + (size_t)kt * 1024),
-                                     reinterpret_cast<void*>(stage + Gm::w_codes + wave * 1024), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(s_src + (size_t)kt * 128),
-                                     reinterpret_cast<void*>(stage + s_dst), 4, 0, 0);
+    if (has_w)
+      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(w_src + (size_t)kt * 1024),
+                                       reinterpret_cast<void*>(stage + Gm::w_codes + wave * 1024), 16, 0, 0);
+    if (has_s)
+      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(s_src + (size_t)kt * 128),
+                                       reinterpret_cast<void*>(stage + s_dst), 4, 0, 0);
   };
-  constexpr int L = 3;   // direct loads per wavefront and stage
+  // direct loads of this wavefront per stage (3 for every wavefront when
+  // there are as many W tiles and scale pairs as wavefronts)
+  constexpr bool kUniformL = Gm::wt == Gm::waves && pairs == Gm::waves;
+  const int L = 1 + (has_w ? 1 : 0) + (has_s ? 1 : 0);
   // prologue: stages (= K steps) 0 .. S-1
 #pragma unroll
   for (int st = 0; st < S; ++st)
@@ -246,9 +254,20 @@ __global__ __launch_bounds__(Gm::threads, 1) void nvfp4_gemm_kernel(
   // `last` issued (the later ones, at most S - 2, may stay in flight)
   auto wait_stage = [&](int need, int last) {
     const int ahead = max(0, min(last, KTi - 1) - need);
-    if (ahead >= 2) wait_vm<2 * L>();
-    else if (ahead == 1) wait_vm<L>();
-    else wait_vm<0>();
+    if constexpr (kUniformL) {
+      if (ahead >= 2) wait_vm<6>();
+      else if (ahead == 1) wait_vm<3>();
+      else wait_vm<0>();
+    } else {
+      switch (ahead * L) {   // loads allowed to stay in flight: 0 .. 2 L, L <= 3
+        case 0: wait_vm<0>(); break;
+        case 1: wait_vm<1>(); break;
+        case 2: wait_vm<2>(); break;
+        case 3: wait_vm<3>(); break;
+        case 4: wait_vm<4>(); break;
+        default: wait_vm<6>(); break;
+      }
+    }
   };
   static_assert(S - 2 <= 2, "wait_stage covers at most two stages in flight");
 
@@ -430,12 +449,14 @@ __global__ __launch_bounds__(Gm::threads, 1) void nvfp4_gemm_kernel(
   }
 }
 
+// Launch geometry Gm over output columns n_off .. n_end-1 (n_off a multiple
+// of 256; n_end a multiple of Gm::bn, or N).
 template <class Gm>
-hipError_t launch_geo(const GemmArgs& a, hipStream_t s) {
+hipError_t launch_geo(const GemmArgs& a, int64_t n_off, int64_t n_end, hipStream_t s) {
   const int64_t a_tiles_r = round_up(a.M, 32) / 32;
   const int64_t w_tiles_r = round_up(a.N, 32) / 32;
   const int64_t KT = round_up(a.K, 64) / 64;
-  const int64_t tiles_m = (a.M + Gm::bm - 1) / Gm::bm, tiles_n = (a.N + Gm::bn - 1) / Gm::bn;
+  const int64_t tiles_m = (a.M + Gm::bm - 1) / Gm::bm, tiles_n = (n_end - n_off + Gm::bn - 1) / Gm::bn;
   const size_t lds = (size_t)Gm::a16_base + 2 * (size_t)Gm::a16_bytes;   // fp4 ring + fp16 A buffers
   static_assert(Gm::a16_base + 2 * Gm::a16_bytes <= kLdsBudget, "LDS budget");
   const bool sw = (a.flags & 1) != 0;
@@ -451,7 +472,7 @@ hipError_t launch_geo(const GemmArgs& a, hipStream_t s) {
     o.tiles_c = round_up(o.Nout, 64) / 64;
   }
   typedef void (*kern_t)(const uint8_t*, const uint8_t*, const float*, const uint8_t*, const uint8_t*, const float*,
-                         int64_t, int64_t, int64_t, int64_t, int64_t, GemmOut, int64_t, int64_t);
+                         int64_t, int64_t, int64_t, int64_t, int64_t, GemmOut, int64_t, int64_t, int64_t);
   static const kern_t kerns[3][2] = {
       {nvfp4_gemm_kernel<Gm, kOutF32, false>, nvfp4_gemm_kernel<Gm, kOutF32, true>},
       {nvfp4_gemm_kernel<Gm, kOutBF16, false>, nvfp4_gemm_kernel<Gm, kOutBF16, true>},
@@ -461,7 +482,8 @@ hipError_t launch_geo(const GemmArgs& a, hipStream_t s) {
                                      (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_m * tiles_n)), dim3(Gm::threads), lds, s, a.A.codes, a.A.scales,
-                     a.A.G, a.W.codes, a.W.scales, a.W.G, a.M, a.N, a_tiles_r, w_tiles_r, KT, o, tiles_m, tiles_n);
+                     a.A.G, a.W.codes, a.W.scales, a.W.G, a.M, a.N, a_tiles_r, w_tiles_r, KT, o, tiles_m, tiles_n,
+                     n_off);
   return hipGetLastError();
 }
 
@@ -476,8 +498,17 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(publish_scale_kernel, dim3(1), dim3(1), 0, s, a.G_out, a.Yq.G);
     return hipGetLastError();
   }
-  // 256x256 workgroup tiles as 2x4 wavefronts of 128x64, two per SIMD
-  return launch_geo<Geo<4, 2, 2, 4, 1>>(a, s);
+  // 256x256 workgroup tiles as 2x4 wavefronts of 128x64, two per SIMD.  One
+  // workgroup fills a CU, so a last round that would leave CUs idle is run
+  // instead as a second launch of half-width (256x128) tiles over the
+  // remaining column panels.
+  using Full = Geo<4, 2, 2, 4, 1>;
+  using Half = Geo<4, 1, 2, 4, 1>;
+  const int64_t n_split = gemm_column_split(a.M, a.N, Full::bm, Full::bn, Half::bn, num_cus());
+  hipError_t e = hipSuccess;
+  if (n_split > 0) e = launch_geo<Full>(a, 0, n_split, s);
+  if (e == hipSuccess && n_split < a.N) e = launch_geo<Half>(a, n_split, a.N, s);
+  return e;
 }
 
 }  // namespace dq
