@@ -293,64 +293,85 @@ __global__ __launch_bounds__(Gm::threads, 1) void nvfp4_gemm_kernel(
   const int a_prd = Gm::a_codes + wave * 1024 + lane * 16;
   const int as_prd = Gm::a_scales + wave * 128 + lane_scale;
 
-  // Producer: A tile `wave` of K step kt, dequantized to fp16 into buffer BUF.
+  // Producer: A tile `wave` of K step kt, dequantized to fp16 into buffer BUF
+  // (the raw tile is read first, so that the reads of a step can be issued
+  // together).
   const bool p_ok = (a_tr0 + wave) < a_tiles_r;
-  auto produce = [&](int kt, auto buf) {
+  struct Raw {
+    uint4_t c;
+    uint32_t sc;
+  };
+  auto produce_read = [&](int kt) -> Raw {
     const uint8_t* stg = smem + (kt % S) * Gm::bytes;
-    const uint4_t c = *reinterpret_cast<const uint4_t*>(stg + a_prd);
-    uint32_t sc = *reinterpret_cast<const uint16_t*>(stg + as_prd);
-    if (!p_ok) sc = 0u;   // a zero scale zeroes the (finite) codes of a missing tile
+    Raw r;
+    r.c = *reinterpret_cast<const uint4_t*>(stg + a_prd);
+    r.sc = *reinterpret_cast<const uint16_t*>(stg + as_prd);
+    return r;
+  };
+  auto produce_write = [&](const Raw& r, auto buf) {
     half2_t s_lo, s_hi;
-    scale_pairs(sc, s_lo, s_hi);
+    scale_pairs(p_ok ? r.sc : 0u, s_lo, s_hi);   // a zero scale zeroes the (finite) codes of a missing tile
 #pragma unroll
     for (int k = 0; k < 4; ++k)
       *reinterpret_cast<half8_t*>(smem + a_wr[k] + decltype(buf)::value * Gm::a16_bytes) =
-          dequant8(c[k], k < 2 ? s_lo : s_hi);
+          dequant8(r.c[k], k < 2 ? s_lo : s_hi);
   };
   auto lgkm0 = [] {
     __builtin_amdgcn_s_waitcnt((0x3F & 0xF) | (0x7 << 4) | (0x0 << 8) | ((0x3F >> 4) << 14));   // lgkmcnt(0)
   };
-  // One K step on A buffer BUF: produce the next step's A into the other
-  // buffer, dequantize this wavefront's W tiles, run the MFMAs; then the
-  // step's barrier (A of step kt+1 written, stage kt+2 landed, stage kt's slot
-  // and buffer BUF free) and the refill of stage kt's slot.
-  auto step = [&](int kt, auto buf) {
+  // MFMA operands of two sub-steps (double buffer): sub-step s of a K step
+  // uses slot s % 2.  The MFMAs of a step's last sub-step are deferred past the
+  // step's barrier: their operands are already in registers, so they keep the
+  // matrix cores busy while the next step's first LDS reads are in flight.
+  half8_t af[2][TM], wf[2][TN];
+  auto mfmas = [&](int slot) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[slot][i], wf[slot][j], acc[i][j], 0, 0, 0);
+  };
+  // One K step on A buffer BUF: read this step's operands and the next
+  // step's raw A tile, finish the previous step (deferred MFMAs), produce the
+  // next step's A into the other buffer, run sub-steps 0..2 (sub-step s+1's
+  // operands are prepared while sub-step s's MFMAs run) and leave sub-step 3
+  // pending; then the step's barrier (A of step kt+1 written, stage kt+2
+  // landed, stage kt's slot and buffer BUF free) and the refill of stage kt's
+  // slot.
+  auto step = [&](int kt, auto buf, auto deferred) {
     using other = std::integral_constant<int, 1 - decltype(buf)::value>;
-    if (kt + 1 < KTi) produce(kt + 1, other{});
+    const bool more = kt + 1 < KTi;
+    Raw raw{};
+    if (more) raw = produce_read(kt + 1);
     const uint8_t* stg = smem + (kt % S) * Gm::bytes;
     uint4_t wc[TN];
-    half2_t ws_[TN][2];
+    uint32_t wsc[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
       wc[j] = *reinterpret_cast<const uint4_t*>(stg + w_rd + j * 1024);
-      uint32_t wsc = *reinterpret_cast<const uint16_t*>(stg + ws_rd + j * 128);
-      if (!w_ok[j]) wsc = 0u;
-      scale_pairs(wsc, ws_[j][0], ws_[j][1]);
+      wsc[j] = *reinterpret_cast<const uint16_t*>(stg + ws_rd + j * 128);
     }
     auto a_frag = [&](int i, int s) -> half8_t {
       return *reinterpret_cast<const half8_t*>(smem + a_rd[s] + decltype(buf)::value * Gm::a16_bytes +
                                                i * Gm::a16_tile);
     };
-    // sub-step s+1's operands (A from LDS, W dequantized) are prepared while
-    // sub-step s's MFMAs run
-    half8_t af[2][TM], wf[2][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i) af[0][i] = a_frag(i, 0);
+    if constexpr (decltype(deferred)::value) mfmas(1);
+    if (more) produce_write(raw, other{});
+    half2_t ws_[TN][2];
 #pragma unroll
-    for (int j = 0; j < TN; ++j) wf[0][j] = dequant8(wc[j][0], ws_[j][0]);
+    for (int j = 0; j < TN; ++j) {
+      scale_pairs(w_ok[j] ? wsc[j] : 0u, ws_[j][0], ws_[j][1]);
+      wf[0][j] = dequant8(wc[j][0], ws_[j][0]);
+    }
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      if (s < 3) {
+    for (int s = 0; s < 3; ++s) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i) af[(s + 1) & 1][i] = a_frag(i, s + 1);
+      for (int i = 0; i < TM; ++i) af[(s + 1) & 1][i] = a_frag(i, s + 1);
 #pragma unroll
-        for (int j = 0; j < TN; ++j) wf[(s + 1) & 1][j] = dequant8(wc[j][s + 1], ws_[j][(s + 1) >> 1]);
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[s & 1][i], wf[s & 1][j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < TN; ++j) wf[(s + 1) & 1][j] = dequant8(wc[j][s + 1], ws_[j][(s + 1) >> 1]);
+      mfmas(s & 1);
     }
     lgkm0();
     if (kt + 2 < KTi) wait_stage(kt + 2, kt + S - 1);
@@ -360,15 +381,20 @@ __global__ __launch_bounds__(Gm::threads, 1) void nvfp4_gemm_kernel(
 
   wait_stage(KTi > 1 ? 1 : 0, S - 1);
   lds_barrier();
-  produce(0, std::integral_constant<int, 0>{});
+  produce_write(produce_read(0), std::integral_constant<int, 0>{});
   lgkm0();
   lds_barrier();
-  int kt = 0;
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  using Yes = std::true_type;
+  step(0, B0{}, std::false_type{});
+  int kt = 1;
   for (; kt + 1 < KTi; kt += 2) {   // A buffers alternate: 0 on even steps, 1 on odd steps
-    step(kt, std::integral_constant<int, 0>{});
-    step(kt + 1, std::integral_constant<int, 1>{});
+    step(kt, B1{}, Yes{});
+    step(kt + 1, B0{}, Yes{});
   }
-  if (kt < KTi) step(kt, std::integral_constant<int, 0>{});
+  if (kt < KTi) step(kt, B1{}, Yes{});
+  mfmas(1);   // the last step's deferred sub-step
 
   const float g = (*Ga) * (*Gw);
   const int col_in = lane & 31;
