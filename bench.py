@@ -45,7 +45,8 @@ METRIC = "NVFP4 prefill GEMM TFLOPS (%FP4 peak); LUT3 decode GEMV GB/s (%HBM pea
 PEAK_FP16_TFLOPS = 2500.0      # dense fp16/bf16 MFMA, MI355X
 PEAK_FP4_TFLOPS = 10100.0      # dense fp4 MFMA, MI355X
 PEAK_HBM_GBS = 8000.0
-GEMM_SOURCE = os.path.join(ROOT, "paper_2609_26333_amd", "csrc", "gemm.hip")
+# sources that decide the GEMM's kernels and launches (tile geometry, column split)
+GEMM_SOURCES = [os.path.join(ROOT, "paper_2609_26333_amd", "csrc", f) for f in ("gemm.hip", "dq_internal.hpp")]
 GEMM_COUNTERS = os.path.join(ROOT, "profiles", "nvfp4_gemm_8b_up_proj_counters.md")
 COPY_BYTES = 256 << 20
 
@@ -64,18 +65,26 @@ def parse():
     return p.parse_args()
 
 
+def gemm_source_sha256():
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
 def gemm_traffic():
-    """HBM bytes per GEMM launch from the committed counter summary: the
-    FETCH_SIZE and WRITE_SIZE readings of the GEMM, each scaled by the bytes
-    a plain copy of known size moves per KiB that the same counter reads.
-    None when the summary is missing or the GEMM source has changed since."""
+    """HBM bytes per GEMM call from the committed counter summary: the
+    FETCH_SIZE and WRITE_SIZE readings of the call's kernel launches (a
+    full-tile launch and, for a partial last round, a half-width-tile launch),
+    each scaled by the bytes a plain copy of known size moves per KiB that the
+    same counter reads.  None when the summary is missing or the GEMM sources
+    have changed since."""
     try:
         text = open(GEMM_COUNTERS).read()
     except OSError:
         return None
     fields = dict(re.findall(r"^- `(\w+)`: `([^`]+)`", text, re.M))
-    sha = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
-    if fields.get("gemm_source_sha256") != sha:
+    if fields.get("gemm_source_sha256") != gemm_source_sha256():
         return None
     try:
         fetch = float(fields["gemm_fetch_kib"]) * float(fields["fetch_bytes_per_kib"])
@@ -301,7 +310,7 @@ def main():
         gbs = nbytes / (per[f"gemv_b{b}"] * 1e-3) / 1e9
         decode[f"b{b}"] = {"us": per[f"gemv_b{b}"] * 1e3, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
                            "bytes": nbytes}
-    # algorithmic bytes of one GEMM launch: the NVFP4 operands once, the bf16 output once
+    # algorithmic bytes of one GEMM call: the NVFP4 operands once, the bf16 output once
     gemm_alg_bytes = M * K * (0.5 + 1 / 16) + N * K * (0.5 + 1 / 16) + M * N * 2
     traffic = gemm_traffic()
 
@@ -321,10 +330,11 @@ def main():
                     "linear_TFLOP/s_incl_quant": prefill_tflops},
         "decode": decode,
         "pack_ms": {"nvfp4": t_pack_nvfp4, "lut3_per_row": t_pack_lut},
-        "roofline": {"bound": "mfma", "kernel": "nvfp4_gemm_kernel", "achieved": gemm_tflops,
+        "roofline": {"bound": "mfma", "kernel": "nvfp4_gemm_kernel (the launches of one dq_prefill_gemm call)",
+                     "achieved": gemm_tflops,
                      "peak": PEAK_FP16_TFLOPS, "unit": "TFLOP/s", "frac": gemm_tflops / PEAK_FP16_TFLOPS,
                      "traffic": traffic,
-                     "traffic_note": (f"HBM bytes per GEMM launch from FETCH_SIZE + WRITE_SIZE (copy-calibrated); "
+                     "traffic_note": (f"HBM bytes per GEMM call from FETCH_SIZE + WRITE_SIZE (copy-calibrated); "
                                       f"algorithmic bytes {gemm_alg_bytes:.4g}" if traffic is not None else
                                       "no counter summary for the current GEMM source"),
                      "note": "exact NVFP4 operands are dequantized to fp16 and multiplied on fp16 MFMA; "
