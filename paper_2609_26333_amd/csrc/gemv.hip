@@ -305,6 +305,13 @@ __device__ inline float group16_max(float m) {
   return m;
 }
 
+// maximum over the wavefront (all 64 lanes must be active)
+__device__ inline float wave_max(float m) {
+  m = group16_max(m);
+  m = fmaxf(m, __shfl_xor(m, 16, 64));
+  return fmaxf(m, __shfl_xor(m, 32, 64));
+}
+
 // Reduce the KS partial sums of each row tile in a fixed order and store
 // (lane: batch column j = lane % 16, rows 4q..4q+3 of the tile).
 __device__ inline void reduce_store(float4_t acc, float4_t* red, int wave, int lane, int ks, int KS, bool tile_ok,
@@ -386,29 +393,24 @@ __global__ __launch_bounds__(1024) void lut_gemv_single_kernel(const uint16_t* _
   __builtin_amdgcn_s_waitcnt((0 & 0xF) | (0x7 << 4) | (0xF << 8));   // vmcnt(0): activations in LDS
   __syncthreads();
 
-  // ---- 2. per-row maxima, then fp16 in place.  A 16-lane group covers 16
-  // consecutive vectors of one batch row (vpr is a multiple of 16).  The row
-  // index f / vpr is exact through fp32: f + 0.5 lies at least 0.5 / vpr away
-  // from a multiple of vpr, far above the rounding error for f < 2^22.
-  const int vpr = KCi * 16, nvec = B * vpr;
-  const float rvpr = 1.0f / (float)vpr;
-  for (int base = wave * 64; base < nvec; base += nthreads) {
-    const int f = base + lane;
-    const int jj = (int)(((float)f + 0.5f) * rvpr), pos = f - jj * vpr;
+  // ---- 2. per-row maxima, then fp16 in place.  Each thread takes the
+  // maximum over its vectors of a batch row, each wavefront reduces it and
+  // makes one LDS atomic per row (atomics on one address serialize).
+  const int vpr = KCi * 16;                 // 8-element vectors per staged row (the zero chunk excluded)
+  const int kvec = (int)(K / 8);            // vectors that hold data (K % 32 == 0); the rest become zero
+  for (int jj = 0; jj < B; ++jj) {
     float m = 0.0f;
-    if (f < nvec && (int64_t)pos * 8 < K) m = max_abs8(*reinterpret_cast<const uint4_t*>(xs + jj * rowstride + pos * 8));
-    m = group16_max(m);
-    if ((lane & 15) == 0 && m > 0.0f) atomicMax(&pmax[jj], __float_as_uint(m));
+    for (int pos = threadIdx.x; pos < kvec; pos += nthreads)
+      m = fmaxf(m, max_abs8(*reinterpret_cast<const uint4_t*>(xs + jj * rowstride + pos * 8)));
+    m = wave_max(m);
+    if (lane == 0 && m > 0.0f) atomicMax(&pmax[jj], __float_as_uint(m));
   }
   __syncthreads();
-  for (int base = wave * 64; base < nvec; base += nthreads) {
-    const int f = base + lane;
-    if (f < nvec) {
-      const int jj = (int)(((float)f + 0.5f) * rvpr), pos = f - jj * vpr;
+  for (int jj = 0; jj < B; ++jj) {
+    const float sc = __builtin_ldexpf(1.0f, stage_exponent(pmax[jj]));
+    for (int pos = threadIdx.x; pos < vpr; pos += nthreads) {
       uint4_t* slot = reinterpret_cast<uint4_t*>(xs + jj * rowstride + pos * 8);
-      const half8_t h = (int64_t)pos * 8 < K ? to_half8_scaled(*slot, __builtin_ldexpf(1.0f, stage_exponent(pmax[jj])))
-                                             : half8_t{};
-      *reinterpret_cast<half8_t*>(slot) = h;
+      *reinterpret_cast<half8_t*>(slot) = pos < kvec ? to_half8_scaled(*slot, sc) : half8_t{};
     }
   }
   __syncthreads();
@@ -524,10 +526,17 @@ __global__ __launch_bounds__(768) void lut_gemv_multi_kernel(const uint16_t* __r
   for (int p = 0; p < NP; ++p) {
     // ---- 2. stage the activation piece: maxima, then fp16
     uint32_t* pm = piece_max[p & 1];
+    // the 64 lanes of a wavefront hold consecutive vectors, so they span a
+    // few consecutive batch rows: one wavefront reduction and one LDS atomic
+    // per row
 #pragma unroll
     for (int n = 0; n < kStageVec; ++n) {
-      const float m = group16_max(max_abs8(v[n]));
-      if ((lane & 15) == 0 && sj[n] < B && m > 0.0f) atomicMax(&pm[sj[n]], __float_as_uint(m));
+      const float m = max_abs8(v[n]);
+      const int r0 = __builtin_amdgcn_readfirstlane(sj[n]), r1 = __builtin_amdgcn_readlane(sj[n], 63);
+      for (int r = r0; r <= r1 && r < B; ++r) {
+        const float mr = wave_max(sj[n] == r ? m : 0.0f);
+        if (lane == 0 && mr > 0.0f) atomicMax(&pm[r], __float_as_uint(mr));
+      }
     }
     if (p == 0) asm volatile("" ::"v"(warm));      // the warm-up loads have landed
     __syncthreads();
