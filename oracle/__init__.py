@@ -14,6 +14,8 @@ What it computes (paper, App. A "Quantization formats"):
   ``max|W| / (6 * 448)``, one E4M3 scale per 16 elements along the
   contraction dimension, E2M1 codes (weights, activations, and the
   requantization of a GEMM output).
+* ``mxfp4``    - MXFP4 (OCP MX: E8M0 power-of-two scale per 32 elements,
+  E2M1 codes), the format of the paper's MXFP4 arms.
 * ``lut``      - LUT weight-only formats: the per-row equal-count LUT fit
   (the benchmark's decode format) and the paper's fixed LUT3A16/LUT2A16
   grids with a signed E4M3 block scale.
@@ -23,4 +25,4 @@ Parity status per function is listed in each module header.  Every
 floating-point step uses IEEE fp32 (NumPy float32, correctly rounded) or
 exact fp64, in the order documented per function.
 """
-from . import formats, nvfp4, lut, linalg  # noqa: F401
+from . import formats, nvfp4, mxfp4, lut, linalg  # noqa: F401

@@ -7,7 +7,8 @@ weight-only LUT formats computes ``y = x @ W_hat^T`` with the bf16
 activations left unquantized (Sec. 2.3; App. C "Kernel specification").
 
 Here both are a float64 ``numpy.matmul`` (BLAS dgemm).  Every product of two
-dequantized NVFP4 values (at most 6 and 4 significant bits) and every
+dequantized NVFP4 values (at most 6 and 4 significant bits), of two MXFP4
+values (at most 2 significant bits each) and every
 product of a bf16 value with an fp16 LUT entry is exact in fp64; only the
 fp64 summation rounds.  Pins (tests/test_oracle_linalg.py): a triple loop
 in exact rational arithmetic on tiny shapes, one-hot rows and columns, and
@@ -17,7 +18,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import formats, lut, nvfp4
+from . import formats, lut, mxfp4, nvfp4
 
 
 def gemm(a_hat, w_hat) -> np.ndarray:
@@ -27,6 +28,10 @@ def gemm(a_hat, w_hat) -> np.ndarray:
 
 def nvfp4_gemm(a_codes, a_scales, G_a, w_codes, w_scales, G_w) -> np.ndarray:
     return gemm(nvfp4.dequantize(a_codes, a_scales, G_a), nvfp4.dequantize(w_codes, w_scales, G_w))
+
+
+def mxfp4_gemm(a_codes, a_scales, w_codes, w_scales) -> np.ndarray:
+    return gemm(mxfp4.dequantize(a_codes, a_scales), mxfp4.dequantize(w_codes, w_scales))
 
 
 def gemv_bf16(x_bits, w_hat) -> np.ndarray:
