@@ -3,7 +3,7 @@
 Thin argument marshalling over the C ABI in ``include/dq.h`` (same call names).
 Every step of the path runs in the gfx950 kernels of ``libdq.so``; there is no
 CPU fallback: importing this package fails if the library is not built
-(``python -m paper_2609_26333_amd.build``).
+(``python paper_2609_26333_amd/build.py``).
 
 PyTorch supplies device memory and the current HIP stream only.
 """
@@ -47,7 +47,7 @@ class _Lut(ctypes.Structure):
 
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_26333_amd.build`")
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2609_26333_amd/build.py`")
     lib = ctypes.CDLL(LIB_PATH)
     P, I64, I32, S = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int32
     SZ = ctypes.POINTER(ctypes.c_size_t)

@@ -1,6 +1,6 @@
 """Build libdq.so (the gfx950 HIP kernels + C ABI) in-tree with hipcc.
 
-Usage: ``python -m paper_2609_26333_amd.build`` (also called by
+Usage: ``python paper_2609_26333_amd/build.py`` (also called by
 ``__graft_entry__.build()``).  Always recompiles.
 """
 from __future__ import annotations
