@@ -17,11 +17,14 @@
 //    pairs: about 1.6 VALU instructions per 3-bit weight;
 //  * the multiply-accumulate runs on MFMA (v_mfma_f32_16x16x32_f16: 16 weight
 //    rows x 32 k x 16 batch columns), so batch 1..16 costs the same VALU work;
-//  * activations are staged once per workgroup into LDS as fp16, rescaled by
-//    a power of two per batch row (exact products with the fp16 table); the
-//    wavefronts of a workgroup split K and reduce through LDS in a fixed
-//    order, so results are deterministic.
+//  * activations are staged into LDS as fp16, rescaled by a power of two
+//    (exact products with the fp16 table); the wavefronts of a workgroup
+//    split K and reduce through LDS in a fixed order, so results are
+//    deterministic.
+// Two kernels: a persistent one (resident workgroups looping over row tiles,
+// whenever the activations fit in LDS) and a piecewise one for larger B*K.
 #include <algorithm>
+#include <atomic>
 #include <cstdint>
 
 #include "dq_device.hpp"
@@ -129,24 +132,16 @@ __device__ inline void table_pools(const uint4_t& d, uint32_t& tl0, uint32_t& tl
   }
 }
 
-// Work decomposition.  A workgroup holds RT row tiles x KS K-splits
-// (W = RT*KS wavefronts); wavefront (rt, ks) consumes chunks ks, ks+KS, ...
-// of row tile rt.  Each wavefront walks a fixed sequence of CPW slots per
-// activation piece (a multiple of its load ring) and keeps RING code loads in
-// flight.  A slot past the end of the piece's chunks re-reads the piece's last
-// chunk and multiplies it by a zero activation chunk instead of branching, so
-// the slot loop has no data-dependent control flow and the compiler can
-// interleave the lookups of one slot with the MFMAs of the previous one.  The
-// KS partial sums of a row tile are reduced through LDS in a fixed order.
-//
-// Two kernels:
-//  * single piece (all of K staged at once; B*K up to ~75 K elements): the
-//    raw activations go straight from global memory into LDS (one wavefront
-//    load per 128-element chunk, no registers held), then are converted in
-//    place; few registers, so several small workgroups share a compute unit;
-//  * several pieces (larger B*K): each piece is staged through registers, and
-//    the next piece's activations are loaded while the current one is
-//    consumed.
+// Piecewise kernel: work decomposition.  A workgroup holds RT row tiles x
+// KS K-splits (W = RT*KS wavefronts); wavefront (rt, ks) consumes chunks ks,
+// ks+KS, ... of row tile rt.  Each wavefront walks a fixed sequence of CPW
+// slots per activation piece (a multiple of its load ring) and keeps RING
+// code loads in flight.  A slot past the end of the piece's chunks re-reads
+// the piece's last chunk and multiplies it by a zero activation chunk instead
+// of branching, so the slot loop has no data-dependent control flow.  The KS
+// partial sums of a row tile are reduced through LDS in a fixed order.  Each
+// activation piece is staged through registers, and the next piece's
+// activations are loaded while the current one is consumed.
 //
 // Memory order.  The weight codes stream from HBM as long row-hit bursts that
 // keep every channel busy; a scattered miss issued behind them (the
@@ -171,6 +166,8 @@ __device__ i32x3_t raw_buffer_load_b96(i32x4_t rsrc, int32_t voff, int32_t soff,
                                        int32_t aux) __asm("llvm.amdgcn.raw.buffer.load.v3i32");
 __device__ int16_t raw_buffer_load_b16(i32x4_t rsrc, int32_t voff, int32_t soff,
                                        int32_t aux) __asm("llvm.amdgcn.raw.buffer.load.i16");
+__device__ int32_t raw_buffer_load_b32(i32x4_t rsrc, int32_t voff, int32_t soff,
+                                       int32_t aux) __asm("llvm.amdgcn.raw.buffer.load.i32");
 
 // gfx9 buffer resource over [p, p + bytes): 48-bit base, stride 0, byte range,
 // 32-bit data format (raw loads ignore the format)
@@ -343,107 +340,299 @@ __device__ inline void reduce_store(float4_t acc, float4_t* red, int wave, int l
   }
 }
 
-constexpr int kRingSingle = 4;
-constexpr int kRingMulti = 8;
 
-// ---------------------------------------------------------------- single piece
-// LDS: B staged rows of (KC + 1) * 128 + 8 fp16 (the last chunk of each row is
-// zero, 8 elements of padding stagger the rows over the banks), then W * 1 KiB
-// for the K-split reduction.
-template <int BITS, int MODE>
-__global__ __launch_bounds__(1024) void lut_gemv_single_kernel(const uint16_t* __restrict__ x, int B, int64_t K,
-                                                               const uint8_t* __restrict__ codes,
-                                                               const uint16_t* __restrict__ lut,
-                                                               const uint8_t* __restrict__ scales,
-                                                               const float* __restrict__ Gp, int64_t N,
-                                                               GemvPlan plan, int out_kind, void* __restrict__ y) {
-  constexpr int RING = kRingSingle;
+// ---------------------------------------------------------------- persistent
+// Resident workgroups that loop over row tiles (used whenever the staged
+// activations fit in LDS).  Workgroup g of G owns row tiles g, g + G, ...
+// ("rounds"); its W wavefronts split every tile's K: wavefront w consumes
+// chunks w, w + W, ... of the tile (CPW = ceil(KC / W) slots per round).
+// Each activation chunk is consumed by exactly one wavefront, which stages it
+// itself: it loads its own raw bf16 chunks straight into LDS, rescales them by
+// a power of two taken from their own maximum (so the fp16 copy is exact for
+// every value within 2^40 of that maximum) and converts them in place; its
+// partial sums are unscaled before the reduction.  Each wavefront also copies
+// the tables of its rounds into a private LDS slot.  Nothing is shared before
+// the reduction, so wavefronts start streaming without a barrier; the code
+// stream is one ring across all rounds.  Partial sums are parked per round
+// and wavefront in LDS; after the single barrier, wavefront r mod W adds the
+// W partials of round r in a fixed order and stores the tile (deterministic).
+struct PersistPlan {
+  int CPW, rounds;
+  int64_t tiles, KC;
+};
+
+// maximum over the 64 lanes (all active) via DPP and lane reads: uniform
+__device__ inline float wave_max_dpp(float v) {
+  int b = __float_as_int(v);
+  b = __float_as_int(fmaxf(__int_as_float(b), __int_as_float(__builtin_amdgcn_mov_dpp(b, 0xB1, 0xF, 0xF, false))));
+  b = __float_as_int(fmaxf(__int_as_float(b), __int_as_float(__builtin_amdgcn_mov_dpp(b, 0x4E, 0xF, 0xF, false))));
+  b = __float_as_int(fmaxf(__int_as_float(b), __int_as_float(__builtin_amdgcn_mov_dpp(b, 0x141, 0xF, 0xF, false))));
+  b = __float_as_int(fmaxf(__int_as_float(b), __int_as_float(__builtin_amdgcn_mov_dpp(b, 0x140, 0xF, 0xF, false))));
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(b, 0)), r1 = __int_as_float(__builtin_amdgcn_readlane(b, 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(b, 32)), r3 = __int_as_float(__builtin_amdgcn_readlane(b, 48));
+  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
+}
+
+template <int BITS, int MODE, int RING, int XREG, int TI>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(6)))
+void lut_gemv_persist_kernel(const uint16_t* __restrict__ x, int B, int64_t K, const uint8_t* __restrict__ codes,
+                             const uint16_t* __restrict__ lut, const uint8_t* __restrict__ scales,
+                             const float* __restrict__ Gp, int64_t N, PersistPlan plan, int out_kind,
+                             void* __restrict__ y) {
+  // Issue arbitration favours older wavefronts: without help the youngest
+  // wavefront of every SIMD stages late and finishes last.  Staging runs at
+  // the top priority, and in the slot loop the priority falls with progress
+  // (3, 2, 1, 0 by quarters), so lagging wavefronts catch up.
+  __builtin_amdgcn_s_setprio(3);
+  typedef typename CodeVec<BITS>::type cvec;
+  constexpr int kChunkBytes = 64 * CodeVec<BITS>::bytes;
+  constexpr int kTabBytes = 16 * 2 * (1 << BITS);     // one row tile's tables
   extern __shared__ __align__(16) uint8_t smem[];
   const int lane = threadIdx.x & 63;
-  // wavefront index as a uniform value: the LDS address of the direct loads
-  // (M0) and all slot bookkeeping stay scalar
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int nthreads = blockDim.x, W = nthreads >> 6;
-  const int KS = plan.KS, rt = wave / KS, ks = wave % KS;
-  const int64_t tile = (int64_t)blockIdx.x * plan.RT + rt;
-  const bool tile_ok = tile < plan.tiles;
-  const int64_t tile_c = tile_ok ? tile : plan.tiles - 1;
-  const int KCi = (int)plan.KC;
-  const int rowstride = (KCi + 1) * 128 + 8;
+  const int W = blockDim.x >> 6;
+  const int KCi = (int)plan.KC, CPW = plan.CPW, R = plan.rounds;
+  const int T = (int)plan.tiles;
+  const int t0 = (int)blockIdx.x * R;              // this workgroup's tiles: t0 .. t0 + nr - 1
+  const int nr = min(R, T - t0);                   // rounds of this workgroup (1 <= nr <= R)
+  const int rowstride = (KCi + 1) * 128 + 8;       // fp16 per staged batch row (+ zero chunk, pad)
+  // LDS: staged activations | partial sums [R][W][64] float4 | tables [W][TI KiB] (PER_ROW)
   _Float16* xs = reinterpret_cast<_Float16*>(smem);
-  float4_t* red = reinterpret_cast<float4_t*>(smem + (size_t)B * rowstride * 2);
-  __shared__ uint32_t pmax[16];
-
-  if ((int)threadIdx.x < 16) pmax[threadIdx.x] = 0u;
-  for (int t = threadIdx.x; t < B * 16; t += nthreads)   // zero chunk of every staged row
-    reinterpret_cast<uint4_t*>(xs + (t >> 4) * rowstride + KCi * 128)[t & 15] = uint4_t{0u, 0u, 0u, 0u};
-
-  // ---- 1. lookup table (lane: row lane % 16 of the tile), and the raw bf16
-  // activations straight into LDS: one wavefront load per 128-element chunk
-  // (lane l: elements 2l, 2l+1; the clamped tail past K is zeroed below)
+  float4_t* part = reinterpret_cast<float4_t*>(smem + (size_t)B * rowstride * 2);
+  uint8_t* tabs = reinterpret_cast<uint8_t*>(part + (size_t)R * W * 64) + (size_t)wave * TI * 1024;
   const int i = lane & 15, j = lane & 15, q = lane >> 4;
-  uint4_t tab{0u, 0u, 0u, 0u};
-  if (tile_ok) tab = load_table<BITS>(MODE == 0 ? lut + (tile * 16 + i) * (1 << BITS) : lut);
-  for (int jj = 0; jj < B; ++jj)
-    for (int c = wave; c < KCi; c += W) {
-      const int64_t k = min((int64_t)c * 128 + 2 * lane, K - 2);
-      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(x + (int64_t)jj * K + k),
-                                       reinterpret_cast<void*>(xs + jj * rowstride + c * 128), 4, 0, 0);
-    }
-  __builtin_amdgcn_s_waitcnt((0 & 0xF) | (0x7 << 4) | (0xF << 8));   // vmcnt(0): activations in LDS
-  __syncthreads();
+  auto tile_of = [&](int r) { return t0 + r; };
 
-  // ---- 2. per-row maxima, then fp16 in place.  Each thread takes the
-  // maximum over its vectors of a batch row, each wavefront reduces it and
-  // makes one LDS atomic per row (atomics on one address serialize).
-  const int vpr = KCi * 16;                 // 8-element vectors per staged row (the zero chunk excluded)
-  const int kvec = (int)(K / 8);            // vectors that hold data (K % 32 == 0); the rest become zero
-  for (int jj = 0; jj < B; ++jj) {
-    float m = 0.0f;
-    for (int pos = threadIdx.x; pos < kvec; pos += nthreads)
-      m = fmaxf(m, max_abs8(*reinterpret_cast<const uint4_t*>(xs + jj * rowstride + pos * 8)));
-    m = wave_max(m);
-    if (lane == 0 && m > 0.0f) atomicMax(&pmax[jj], __float_as_uint(m));
-  }
-  __syncthreads();
-  for (int jj = 0; jj < B; ++jj) {
-    const float sc = __builtin_ldexpf(1.0f, stage_exponent(pmax[jj]));
-    for (int pos = threadIdx.x; pos < vpr; pos += nthreads) {
-      uint4_t* slot = reinterpret_cast<uint4_t*>(xs + jj * rowstride + pos * 8);
-      *reinterpret_cast<half8_t*>(slot) = pos < kvec ? to_half8_scaled(*slot, sc) : half8_t{};
-    }
-  }
-  __syncthreads();
-  const bool xlane = j < B;
-  const float unscale = xlane ? __builtin_ldexpf(1.0f, -stage_exponent(pmax[j])) : 1.0f;
-
-  // ---- 3. the first RING code loads, once the activations are staged: while
-  // every compute unit starts its weight stream, issuing a load can stall on
-  // back-pressure, which must not hold up the staging barriers
-  CodeStream<BITS, MODE, RING> cs;
-  cs.init(codes + tile_c * plan.KC * CodeStream<BITS, MODE, RING>::kChunkBytes,
-          MODE == 1 ? scales + tile_c * plan.KC * 128 : nullptr, lane, KCi, KS, ks, KCi);
+  // ---- 1. this wavefront's activation chunks (lane l: elements 2l, 2l+1 of
+  // each chunk), and the tables of its rounds.  Batch 1 with at most XREG
+  // chunks per wavefront: into registers through a range-checked buffer
+  // resource (reads past K return zero).  Otherwise raw into LDS, with reads
+  // past K clamped in bounds and zeroed at conversion.
+  const int nxc = (KCi - wave + W - 1) / W;        // chunks of this wavefront
+  constexpr bool xreg = XREG > 0;   // the host guarantees B == 1 and nxc <= XREG
+  uint32_t xr[XREG > 0 ? XREG : 1];
+  if constexpr (xreg) {
+    const i32x4_t rx = buffer_resource(x, (uint32_t)(K * 2));
 #pragma unroll
-  for (int r = 0; r < RING; ++r) cs.load(r, cs.chunk(0, r));
+    for (int u = 0; u < (XREG > 0 ? XREG : 1); ++u)
+      xr[u] = (uint32_t)raw_buffer_load_b32(rx, lane * 4, ((u * W + wave) * 128) * 2, 0);
+  } else {
+    for (int jj = 0; jj < B; ++jj)
+      for (int c = wave; c < KCi; c += W) {
+        const int64_t k = min((int64_t)c * 128 + 2 * lane, K - 2);
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(x + (int64_t)jj * K + k),
+                                         reinterpret_cast<void*>(xs + jj * rowstride + c * 128), 4, 0, 0);
+      }
+  }
+  if (MODE == 0) {
+    // the tables of tiles t0 .. are contiguous: TI KiB per wavefront (a fixed
+    // count of loads, so that the compiler's load counting stays exact);
+    // reads past the table array return zero
+    const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(lut), 0, (int)((int64_t)T * kTabBytes), 0x00020000);
+#pragma unroll
+    for (int ti = 0; ti < TI; ++ti)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (__attribute__((address_space(3))) void*)(tabs + ti * 1024), 16,
+                                               lane * 16, t0 * kTabBytes + ti * 1024, 0, 0);
+  }
+  uint4_t grid_tab{0u, 0u, 0u, 0u};
+  if (MODE == 1) grid_tab = load_table<BITS>(lut);
 
-  // ---- 4. slots
+  // ---- 2. the first RING code loads (and block-scale pairs).  Slot cursor
+  // (round r, step s) -> chunk s*W + wave of tile g + r*G; past the last slot
+  // the cursor stays on it (harmless re-reads keep the ring unconditional)
+  const i32x4_t rcodes = buffer_resource(codes, (uint32_t)T * (uint32_t)KCi * kChunkBytes);
+  i32x4_t rscales{};
+  if (MODE == 1) rscales = buffer_resource(scales, (uint32_t)T * (uint32_t)KCi * 128);
+  const int32_t lane_code = lane * CodeVec<BITS>::bytes, lane_scale = lane * 2;
+  cvec ring[RING];
+  uint32_t sring[RING];
+  int lr = 0, ls = 0;   // load cursor
+  auto load_next = [&](int slot) {
+    const int cidx = tile_of(lr) * KCi + min(ls * W + wave, KCi - 1);
+    if constexpr (BITS == 3) {
+      const i32x3_t v = raw_buffer_load_b96(rcodes, lane_code, cidx * kChunkBytes, 0);
+      ring[slot] = cvec{{(uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2]}};
+    } else {
+      const i32x2_t v = raw_buffer_load_b64(rcodes, lane_code, cidx * kChunkBytes, 0);
+      ring[slot] = cvec{{(uint32_t)v[0], (uint32_t)v[1]}};
+    }
+    if (MODE == 1) sring[slot] = (uint16_t)raw_buffer_load_b16(rscales, lane_scale, cidx * 128, 0);
+    if (++ls == CPW) {
+      ls = 0;
+      ++lr;
+    }
+    if (lr == nr) {   // stay on the last slot
+      lr = nr - 1;
+      ls = CPW - 1;
+    }
+  };
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int r = 0; r < RING; ++r) load_next(r);
+  __builtin_amdgcn_sched_barrier(0);
+  // the zero chunk of every staged row (each wavefront writes the same zeros)
+  for (int jj = 0; jj < B; ++jj) reinterpret_cast<uint32_t*>(xs + jj * rowstride + KCi * 128)[lane] = 0u;
+
+  // ---- 3. once its own loads have landed (vmcnt: the code loads may still
+  // be in flight), the wavefront rescales and converts its chunks in place
+  {
+    constexpr int kv = RING * (MODE == 1 ? 2 : 1) + (MODE == 0 ? TI : 1);
+    __builtin_amdgcn_s_waitcnt((kv & 0xF) | ((kv >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  float unscale = 1.0f;
+  // the scaled values are exact in fp16, so the conversion's rounding mode
+  // is immaterial
+  auto to_h2 = [](uint32_t v, float sc) {
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(bf16_lo(v) * sc, bf16_hi(v) * sc));
+  };
+  if constexpr (xreg) {
+    float m = 0.0f;
+#pragma unroll
+    for (int u = 0; u < (XREG > 0 ? XREG : 1); ++u) m = fmaxf(m, fmaxf(fabsf(bf16_lo(xr[u])), fabsf(bf16_hi(xr[u]))));
+    const int e = stage_exponent(__float_as_uint(wave_max_dpp(m)));
+    const float sc = __builtin_ldexpf(1.0f, e);
+    unscale = __builtin_ldexpf(1.0f, -e);
+    uint32_t* row = reinterpret_cast<uint32_t*>(xs) + lane;
+#pragma unroll
+    for (int u = 0; u < (XREG > 0 ? XREG : 1); ++u)
+      if (u < nxc) row[(u * W + wave) * 64] = to_h2(xr[u], sc);
+  } else {
+    // batches of 8 chunks, so that the LDS round trips overlap
+    for (int jj = 0; jj < B; ++jj) {
+      uint32_t* row = reinterpret_cast<uint32_t*>(xs + jj * rowstride) + lane;
+      float m = 0.0f;
+      for (int t0 = 0; t0 < nxc; t0 += 8) {
+        uint32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = t0 + u < nxc ? row[((t0 + u) * W + wave) * 64] : 0u;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) m = fmaxf(m, fmaxf(fabsf(bf16_lo(v[u])), fabsf(bf16_hi(v[u]))));
+      }
+      const int e = stage_exponent(__float_as_uint(wave_max_dpp(m)));
+      const float sc = __builtin_ldexpf(1.0f, e);
+      if (j == jj) unscale = __builtin_ldexpf(1.0f, -e);
+      for (int t0 = 0; t0 < nxc; t0 += 8) {
+        uint32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = t0 + u < nxc ? row[((t0 + u) * W + wave) * 64] : 0u;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int c = (t0 + u) * W + wave;
+          if (t0 + u < nxc) row[c * 64] = (int64_t)c * 128 + 2 * lane < K ? to_h2(v[u], sc) : 0u;
+        }
+      }
+    }
+  }
+  const bool xlane = j < B;
+  if (MODE == 1) unscale *= *Gp;
+  auto round_table = [&](int r) {
+    if (MODE == 1) return grid_tab;
+    const uint8_t* t = tabs + r * kTabBytes + i * 2 * (1 << BITS);   // r < TI KiB / kTabBytes
+    if (BITS == 3) return *reinterpret_cast<const uint4_t*>(t);
+    const uint2_t d = *reinterpret_cast<const uint2_t*>(t);
+    return uint4_t{d[0], d[1], 0u, 0u};
+  };
+
+  // ---- 4. slots: RING loads in flight across rounds.  The table copies
+  // were issued just before the ring: wait for them (the compiler does not
+  // track loads into LDS); later rounds' tables have landed by the time the
+  // round's first ring slot has
+  if (MODE == 0) {
+    __builtin_amdgcn_s_waitcnt((RING & 0xF) | ((RING >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  uint32_t tl0, tl1, th0, th1;
+  table_pools<BITS>(round_table(0), tl0, tl1, th0, th1);
   float4_t pacc[4];
 #pragma unroll
   for (int st = 0; st < 4; ++st) pacc[st] = float4_t{0.f, 0.f, 0.f, 0.f};
   // batch columns >= B read row 0: their MFMA output columns are never stored
   const _Float16* xrow = xs + (xlane ? j : 0) * rowstride + 32 * q;
-  consume<BITS, MODE, RING>(cs, 0, 0, plan.CPW, xrow, tile_ok ? 0 : KCi, tab, pacc);
-  float4_t acc;
+  const int total = nr * CPW;
+  int rd = 0, s = 0;   // consume cursor
+  const int q1 = total / 4, q2 = total / 2, q3 = (3 * total) / 4;
+  for (int f0 = 0; f0 < total; f0 += RING) {
+    if (f0 >= q3)
+      __builtin_amdgcn_s_setprio(0);
+    else if (f0 >= q2)
+      __builtin_amdgcn_s_setprio(1);
+    else if (f0 >= q1)
+      __builtin_amdgcn_s_setprio(2);
 #pragma unroll
-  for (int r2 = 0; r2 < 4; ++r2) acc[r2] = ((pacc[0][r2] + pacc[1][r2]) + (pacc[2][r2] + pacc[3][r2])) * unscale;
-  if (MODE == 1) {
-    const float g = *Gp;
+    for (int r = 0; r < RING; ++r) {
+      if (f0 + r >= total) break;   // past the last slot (uniform)
+      const int c = s * W + wave;
+      const int xc = (rd < nr && c < KCi) ? c : KCi;   // past the end: the zero chunk
+      half8_t bf[4];
+      const half8_t* xp = reinterpret_cast<const half8_t*>(xrow + xc * 128);
 #pragma unroll
-    for (int r2 = 0; r2 < 4; ++r2) acc[r2] *= g;
+      for (int st = 0; st < 4; ++st) bf[st] = xp[st];
+      const uint32_t sv = sring[r];
+      uint32_t sel[8];
+      selectors<BITS>(ring[r], sel);
+      load_next(r);
+      half2_t s_lo, s_hi;
+      if (MODE == 1) {
+        const half2_t sc2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sv, 1.0f, false);
+        s_lo = half2_t{sc2[0], sc2[0]};
+        s_hi = half2_t{sc2[1], sc2[1]};
+      }
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        uint32_t a0, a1, a2, a3;
+        lookup4(sel[2 * st], tl0, tl1, th0, th1, a0, a1);
+        lookup4(sel[2 * st + 1], tl0, tl1, th0, th1, a2, a3);
+        half8_t af = as_half8(a0, a1, a2, a3);
+        if (MODE == 1) af = scale_half8(af, st < 2 ? s_lo : s_hi);
+        pacc[st] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf[st], pacc[st], 0, 0, 0);
+      }
+      if (++s == CPW) {
+        s = 0;
+        if (rd < nr) {   // end of round rd: park the partial sums
+          float4_t acc;
+#pragma unroll
+          for (int r2 = 0; r2 < 4; ++r2)
+            acc[r2] = ((pacc[0][r2] + pacc[1][r2]) + (pacc[2][r2] + pacc[3][r2])) * unscale;
+#pragma unroll
+          for (int st = 0; st < 4; ++st) pacc[st] = float4_t{0.f, 0.f, 0.f, 0.f};
+          part[((size_t)rd * W + wave) * 64 + lane] = acc;
+          if (rd + 1 < nr) table_pools<BITS>(round_table(rd + 1), tl0, tl1, th0, th1);
+        }
+        ++rd;
+      }
+    }
   }
-  // ---- 5. K-split reduction and store
-  reduce_store(acc, red, wave, lane, ks, KS, tile_ok, tile, N, out_kind, y, xlane);
+  // ---- 5. reduce each round's W partials in order and store the tile
+  __syncthreads();
+  for (int r = wave; r < nr; r += W) {
+    if (!xlane) continue;
+    const float4_t* pr = part + (size_t)r * W * 64 + lane;
+    float4_t o = pr[0];
+    for (int w2 = 1; w2 < W; ++w2) {
+      const float4_t t2 = pr[w2 * 64];
+      o[0] += t2[0];
+      o[1] += t2[1];
+      o[2] += t2[2];
+      o[3] += t2[3];
+    }
+    const int64_t tile = tile_of(r);
+#pragma unroll
+    for (int r2 = 0; r2 < 4; ++r2) {
+      const int64_t row = tile * 16 + 4 * q + r2;
+      if (row < N) {
+        const int64_t o2 = (int64_t)j * N + row;
+        if (out_kind == 0)
+          reinterpret_cast<float*>(y)[o2] = o[r2];
+        else
+          reinterpret_cast<uint16_t*>(y)[o2] = (uint16_t)f32_to_bf16_rne(o[r2]);
+      }
+    }
+  }
 }
+
+constexpr int kRingMulti = 8;
 
 // ---------------------------------------------------------------- several pieces
 template <int BITS, int MODE>
@@ -471,7 +660,8 @@ __global__ __launch_bounds__(768) void lut_gemv_multi_kernel(const uint16_t* __r
 
   // Staging assignment, fixed for the kernel: vector n of this thread is
   // elements [8*spos, 8*spos + 8) of batch row sj of every piece (valid when
-  // sj < B); the division is exact as in the single-piece kernel.
+  // sj < B); ((f + 0.5) / vpr in fp32 truncates to the exact quotient for
+  // these small operands).
   int sj[kStageVec], spos[kStageVec];
   {
     const float rvpr = 1.0f / (float)vpr;
@@ -580,8 +770,21 @@ __global__ void zero_fill_kernel(uint32_t* p, int64_t n) {
 }
 
 constexpr int64_t kLdsPerCu = 160 * 1024;
-constexpr int64_t kSingleLdsMax = 148 * 1024;   // staged activations of the single-piece kernel
 constexpr int kCUs = 256;
+
+constexpr int kRingPersist = 4;
+constexpr int64_t kPersistLdsMax = 150 * 1024;
+
+// Workgroups of `waves` wavefronts that one compute unit holds at once: the
+// waves of a workgroup are spread evenly over the 4 SIMDs, so each SIMD needs
+// room for ceil(waves / 4) of them (a SIMD holds 512 / VGPRs-per-wave, at
+// most 8), and the LDS must hold all of them.
+inline int persist_wgs_per_cu(int vgprs, int waves, int64_t lds) {
+  const int per_simd = std::min(8, 512 / (int)round_up(vgprs, 8));
+  const int by_vgpr = per_simd / ((waves + 3) / 4);
+  const int by_lds = (int)(kLdsPerCu / std::max<int64_t>(1, lds + 1024));
+  return std::max(1, std::min(by_vgpr, by_lds));
+}
 
 template <int BITS, int MODE>
 hipError_t launch_gemv_t(const uint16_t* x, int64_t B, const LutView& w, int out_kind, void* y, hipStream_t s) {
@@ -589,45 +792,64 @@ hipError_t launch_gemv_t(const uint16_t* x, int64_t B, const LutView& w, int out
   GemvPlan pl{};
   pl.tiles = round_up(N, 16) / 16;
   pl.KC = round_up(K, 128) / 128;
-  const int64_t lds_single = B * ((pl.KC + 1) * 128 + 8) * 2;
-  if (lds_single <= kSingleLdsMax) {
-    // Single piece.  Measured on the decode shapes: the best splits put
-    // about 12 wavefronts per compute unit in all (KS ~ 3072 / tiles K-splits
-    // per row tile), with a K-split that wastes few ring slots, and 2-3 row
-    // tiles per workgroup so that the activation staging is shared, while
-    // keeping at least one workgroup per compute unit where the row tiles
-    // allow it.
-    const int64_t ks0 = std::min<int64_t>(std::min<int64_t>(16, pl.KC), std::max<int64_t>(1, (3072 + pl.tiles - 1) / pl.tiles));
-    double best = 1e300;
-    for (int64_t ks = std::max<int64_t>(1, ks0 - 3); ks <= std::min<int64_t>(std::min<int64_t>(16, pl.KC), ks0 + 3); ++ks)
-      for (int rt = 3; rt >= 1; --rt) {
-        if (rt * ks > 16) continue;
-        const int64_t cpw = round_up((pl.KC + ks - 1) / ks, kRingSingle);
-        const int64_t G = (pl.tiles + rt - 1) / rt;
-        double score = (double)(cpw * ks) / (double)pl.KC;               // slot waste
-        score *= 1.0 + 0.05 * (double)std::abs(ks - ks0);                 // distance from the wavefront target
-        if (rt == 1) score *= 1.3;                                        // staging not shared
-        if (G < kCUs && rt > 1) score *= 1.0 + 0.3 * (1.0 - (double)G / kCUs);   // idle compute units
-        // workgroups that fit one compute unit's LDS at once: a partial extra
-        // round of workgroups costs a whole one
-        const int64_t slots = kCUs * std::max<int64_t>(1, kLdsPerCu / (lds_single + rt * ks * 1024));
-        if (G > slots) score *= (double)((G + slots - 1) / slots) / ((double)G / (double)slots);
-        if (score < best * 0.999) {
-          best = score;
-          pl.RT = rt;
-          pl.KS = (int)ks;
-          pl.CPW = (int)cpw;
-        }
+  // Persistent kernel whenever the staged activations leave room for at
+  // least one workgroup per compute unit and a workgroup needs at most 8
+  // rounds (2 KiB of tables per wavefront).
+  {
+    constexpr int kW = 8;
+    constexpr int kTabBytes = 32 << BITS;
+    const int64_t code_bytes = pl.tiles * pl.KC * 64 * (BITS == 3 ? 12 : 8);
+    const int64_t cpw = (pl.KC + kW - 1) / kW;
+    const int xv = B == 1 && cpw <= 8 ? 0 : B == 1 && cpw <= 18 ? 1 : 2;   // activation staging variant
+    auto table_kib = [&](int64_t rounds) { return (rounds * kTabBytes + 1023) / 1024; };
+    // LDS: staged activations, per round W partial sums, W table copies
+    auto lds_of = [&](int64_t rounds) {
+      return B * ((pl.KC + 1) * 128 + 8) * 2 + rounds * kW * 1024 + (MODE == 0 ? kW * table_kib(rounds) * 1024 : 0);
+    };
+    typedef void (*kern_t)(const uint16_t*, int, int64_t, const uint8_t*, const uint16_t*, const uint8_t*,
+                           const float*, int64_t, PersistPlan, int, void*);
+    auto pick = [&](int ti) -> kern_t {
+      if (ti <= 1)
+        return xv == 0 ? lut_gemv_persist_kernel<BITS, MODE, kRingPersist, 8, 1>
+               : xv == 1 ? lut_gemv_persist_kernel<BITS, MODE, kRingPersist, 18, 1>
+                         : lut_gemv_persist_kernel<BITS, MODE, kRingPersist, 0, 1>;
+      return xv == 0 ? lut_gemv_persist_kernel<BITS, MODE, kRingPersist, 8, 2>
+             : xv == 1 ? lut_gemv_persist_kernel<BITS, MODE, kRingPersist, 18, 2>
+                       : lut_gemv_persist_kernel<BITS, MODE, kRingPersist, 0, 2>;
+    };
+    if (lds_of(1) <= kPersistLdsMax && code_bytes < ((int64_t)1 << 31)) {
+      // VGPRs of the kernels (the same for every table count), queried once
+      static std::atomic<int> vgprs_of[3];
+      std::atomic<int>& vgprs = vgprs_of[xv];
+      if (vgprs.load(std::memory_order_relaxed) == 0) {
+        hipFuncAttributes a{};
+        vgprs.store(hipFuncGetAttributes(&a, reinterpret_cast<const void*>(pick(1))) == hipSuccess && a.numRegs > 0
+                        ? a.numRegs : 128, std::memory_order_relaxed);
       }
-    pl.PK = (int)pl.KC;
-    pl.npieces = 1;
-    const int W = pl.RT * pl.KS;
-    const size_t lds = (size_t)lds_single + (size_t)W * 1024;
-    const int64_t blocks = (pl.tiles + pl.RT - 1) / pl.RT;
-    hipLaunchKernelGGL((lut_gemv_single_kernel<BITS, MODE>), dim3((unsigned)blocks), dim3(W * 64), lds, s, x,
-                       (int)B, K, w.codes, w.lut, w.scales, w.G, N, pl, out_kind, y);
-    return hipGetLastError();
+      // rounds: one per resident workgroup slot, every workgroup running the
+      // same number (a partial last round would leave few wavefronts
+      // streaming at the end)
+      int64_t rounds = 1;
+      for (int it = 0; it < 3; ++it) {
+        const int per_cu = persist_wgs_per_cu(vgprs.load(std::memory_order_relaxed), kW, lds_of(rounds));
+        const int64_t gmax = std::max<int64_t>(1, (int64_t)num_cus() * per_cu);
+        rounds = (pl.tiles + gmax - 1) / gmax;
+      }
+      const int ti = (int)table_kib(rounds);
+      if (lds_of(rounds) <= kPersistLdsMax && (MODE == 1 || ti <= 2)) {
+        PersistPlan pp{};
+        pp.tiles = pl.tiles;
+        pp.KC = pl.KC;
+        pp.CPW = (int)cpw;
+        pp.rounds = (int)rounds;
+        const int64_t G = (pl.tiles + rounds - 1) / rounds;
+        hipLaunchKernelGGL(pick(ti), dim3((unsigned)G), dim3(kW * 64), (size_t)lds_of(rounds), s, x, (int)B, K,
+                           w.codes, w.lut, w.scales, w.G, N, pp, out_kind, y);
+        return hipGetLastError();
+      }
+    }
   }
+pieces:
   // Several pieces.  Row tiles per workgroup: the workgroups must spread
   // evenly over the compute units (cost = rounds x row tiles per workgroup);
   // ties go to more row tiles per workgroup, which amortizes the staging.  K
