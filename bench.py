@@ -167,11 +167,15 @@ def decode_sweep(dq, synth, torch, np, n_blocks, steps):
             ys = [torch.empty((B, l.n), dtype=torch.float32, device="cuda") for l in cfg.layers]
             xp = [ctypes.c_void_p(t.data_ptr()) for t in xs]
             yp = [ctypes.c_void_p(t.data_ptr()) for t in ys]
+            ws_n = max(dq.dq_decode_gemv_workspace_size(B, l) for l in block)
+            ws = torch.empty(max(ws_n, 16), dtype=torch.uint8, device="cuda")
+            wsp = ctypes.c_void_p(ws.data_ptr())
 
             def token():
                 for d in descs:
                     for i in range(len(cfg.layers)):
-                        assert lib.dq_decode_gemv(xp[i], B, ctypes.byref(d[i]), dq.OUT_F32, yp[i], sp) == 0
+                        assert lib.dq_decode_gemv(xp[i], B, ctypes.byref(d[i]), dq.OUT_F32, yp[i], wsp, ws_n,
+                                                  sp) == 0
             token()
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -264,9 +268,13 @@ def main():
         return lib.dq_prefill_gemm(ctypes.byref(dA), None, None, ctypes.byref(dW), M, dq.OUT_BF16,
                                    ctypes.c_void_p(Y.data_ptr()), None, None, 0, sp)
 
+    ws_n = max(dq.dq_decode_gemv_workspace_size(b, Wls[0]) for b in Bs)
+    ws = torch.empty(max(ws_n, 16), dtype=torch.uint8, device="cuda")
+    wsp = ctypes.c_void_p(ws.data_ptr())
+
     def gemv(i, b):
         return lib.dq_decode_gemv(ctypes.c_void_p(xd_dev[b].data_ptr()), b, ctypes.byref(dWls[i % n_w]),
-                                  dq.OUT_F32, ctypes.c_void_p(ys[b].data_ptr()), sp)
+                                  dq.OUT_F32, ctypes.c_void_p(ys[b].data_ptr()), wsp, ws_n, sp)
 
     names = ["quant", "gemm"] + [f"gemv_b{b}" for b in Bs]
 

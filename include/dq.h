@@ -9,8 +9,10 @@
  *
  * Conventions for every call
  *   - Buffers are device memory owned by the caller.  The library keeps no
- *     state except a thread-local last-error string, and allocates nothing
- *     except the stream-ordered staging of dq_prefill_gemm's fused path.
+ *     state except a thread-local last-error string and a per-device memory
+ *     pool, from which it takes stream-ordered staging only for
+ *     dq_prefill_gemm's fused path and for dq_decode_gemv called without a
+ *     workspace.
  *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*;
  *     NULL is the default stream).  Nothing synchronizes inside the library.
  *   - Arguments are validated on the host before any HIP call; a rejected
@@ -33,7 +35,7 @@
 extern "C" {
 #endif
 
-#define DQ_ABI_VERSION 1
+#define DQ_ABI_VERSION 2
 
 typedef int32_t dq_status;
 #define DQ_OK 0
@@ -202,16 +204,27 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
                           void* stream);
 
 /* ---- a6: weight-only LUT GEMV (decode; no activation quantization) -------
+ * The weight-only path the paper serves decode with (Sec. 3 "Format
+ * disaggregation"; time set by the weight bytes streamed per token, Sec. 5).
  * y[b, n] = sum_k x[b, k] * w_hat[n, k], fp32 accumulation.
  * x: device bf16 [B, K] row-major, 1 <= B <= 16.  W: packed LUT weight.
  * out_kind DQ_OUT_F32 / DQ_OUT_BF16: y is device [B, N] row-major.
- * Activations are converted to fp16 inside the kernel after a per-row
- * power-of-two rescale (exact for every bf16 value within 2^40 of the row's
- * largest magnitude); products with the fp16 table are exact.  In PAPER_GRID
- * mode the block scale is folded into the fp16 operand (one rounding,
- * relative 2^-11 per weight). */
+ * workspace: device memory of at least dq_decode_gemv_workspace_size() bytes
+ *   (16-byte aligned), used for split-K partial sums when B >= 2; it must not
+ *   be in use by other work while the call runs on `stream`.  NULL: the
+ *   library takes it from its own pool, stream-ordered (costs ~10 us of host
+ *   time per call).  workspace_bytes below the required size is rejected.
+ * Activations are converted to fp16 inside the kernel after a power-of-two
+ * rescale from the largest magnitude of the slice of x that one wavefront
+ * (B = 1) or one K group of a batch row (B >= 2) reads; a bf16 value is
+ * converted exactly unless it lies more than 2^24 below that magnitude (it
+ * then rounds as an fp16 subnormal).  Products with the fp16 table are
+ * exact; partial sums are scaled back by the same power of two.  In
+ * PAPER_GRID mode the block scale is folded into the fp16 operand (one
+ * rounding, relative 2^-11 per weight). */
+dq_status dq_decode_gemv_workspace_size(int64_t B, const dq_lut_t* W, size_t* bytes);
 dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y,
-                         void* stream);
+                         void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

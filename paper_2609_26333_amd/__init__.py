@@ -62,7 +62,8 @@ def _load() -> ctypes.CDLL:
         "dq_quantize_act_nvfp4": (S, [P, I64, I64, P, ctypes.POINTER(_NvFp4), P]),
         "dq_prefill_gemm": (S, [ctypes.POINTER(_NvFp4), P, P, ctypes.POINTER(_NvFp4), I64, I32, P, P,
                                 ctypes.POINTER(_NvFp4), I32, P]),
-        "dq_decode_gemv": (S, [P, I64, ctypes.POINTER(_Lut), I32, P, P]),
+        "dq_decode_gemv_workspace_size": (S, [I64, ctypes.POINTER(_Lut), SZ]),
+        "dq_decode_gemv": (S, [P, I64, ctypes.POINTER(_Lut), I32, P, P, ctypes.c_size_t, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -73,7 +74,8 @@ def _load() -> ctypes.CDLL:
 
 _lib = _load()
 EXPORTED = ("dq_abi_version", "dq_status_string", "dq_last_error", "dq_nvfp4_sizes", "dq_lut_sizes",
-            "dq_pack_nvfp4", "dq_pack_lut3", "dq_quantize_act_nvfp4", "dq_prefill_gemm", "dq_decode_gemv")
+            "dq_pack_nvfp4", "dq_pack_lut3", "dq_quantize_act_nvfp4", "dq_prefill_gemm",
+            "dq_decode_gemv_workspace_size", "dq_decode_gemv")
 
 
 def lib() -> ctypes.CDLL:
@@ -235,17 +237,39 @@ def dq_prefill_gemm(W: NvFp4Tensor, A: Optional[NvFp4Tensor] = None, X: Optional
     return Yq if out_kind == OUT_NVFP4 else Y
 
 
+_gemv_ws_cache: dict = {}
+
+
+def dq_decode_gemv_workspace_size(B: int, W: LutWeight) -> int:
+    """Workspace bytes dq_decode_gemv needs for batch B (0 for B = 1)."""
+    key = (B, W.rows, W.cols, W.bits, W.mode, W.codes.device.index)
+    n = _gemv_ws_cache.get(key)
+    if n is None:
+        out = ctypes.c_size_t()
+        _check(_lib.dq_decode_gemv_workspace_size(B, ctypes.byref(W.desc()), ctypes.byref(out)),
+               "dq_decode_gemv_workspace_size")
+        n = _gemv_ws_cache[key] = out.value
+    return n
+
+
 def dq_decode_gemv(x: torch.Tensor, W: LutWeight, out_kind: int = OUT_F32, y: Optional[torch.Tensor] = None,
-                   stream=None) -> torch.Tensor:
+                   stream=None, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
     x = _as_u16(x)
     assert x.is_contiguous() and x.dim() == 2
     B = x.shape[0]
     if y is None:
         y = torch.empty((B, W.rows), dtype=torch.float32 if out_kind == OUT_F32 else torch.bfloat16,
                         device=x.device)
+    if workspace is None:
+        # torch's caching allocator hands out stream-ordered memory
+        n = dq_decode_gemv_workspace_size(B, W)
+        if n:
+            workspace = torch.empty(n, dtype=torch.uint8, device=x.device)
+    ws_ptr, ws_bytes = (workspace.data_ptr(), workspace.numel() * workspace.element_size()) if workspace is not None \
+        else (None, 0)
     d = W.desc()
-    _check(_lib.dq_decode_gemv(x.data_ptr(), B, ctypes.byref(d), out_kind, y.data_ptr(), _stream(stream)),
-           "dq_decode_gemv")
+    _check(_lib.dq_decode_gemv(x.data_ptr(), B, ctypes.byref(d), out_kind, y.data_ptr(), ws_ptr, ws_bytes,
+                               _stream(stream)), "dq_decode_gemv")
     return y
 
 

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <mutex>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -94,6 +95,33 @@ int num_cus() {
   if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
   cached[dev].store(n, std::memory_order_relaxed);
   return n;
+}
+
+hipError_t pool_alloc_async(void** p, size_t bytes, hipStream_t s) {
+  static std::atomic<hipMemPool_t> pools[64];
+  static std::mutex mu;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipMallocAsync(p, bytes, s);
+  hipMemPool_t pool = pools[dev].load(std::memory_order_acquire);
+  if (pool == nullptr) {
+    std::lock_guard<std::mutex> lock(mu);
+    pool = pools[dev].load(std::memory_order_relaxed);
+    if (pool == nullptr) {
+      hipMemPoolProps props{};
+      props.allocType = hipMemAllocationTypePinned;
+      props.location.type = hipMemLocationTypeDevice;
+      props.location.id = dev;
+      e = hipMemPoolCreate(&pool, &props);
+      if (e != hipSuccess) return e;
+      uint64_t keep = UINT64_MAX;   // never trim: later calls reuse the memory
+      e = hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+      if (e != hipSuccess) return e;
+      pools[dev].store(pool, std::memory_order_release);
+    }
+  }
+  return hipMallocFromPoolAsync(p, bytes, pool, s);
 }
 
 }  // namespace dq
@@ -248,7 +276,7 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
     const int64_t r = rup(M, 32), c = rup(K, 64);
     const size_t code_bytes = (size_t)(r * c / 2), scale_bytes = (size_t)(r * c / 16);
     const size_t bytes = code_bytes + scale_bytes + 16;
-    hipError_t e = hipMallocAsync(&staging, bytes, hs);
+    hipError_t e = dq::pool_alloc_async(&staging, bytes, hs);
     if (e != hipSuccess) return hip_status(e, "dq_prefill_gemm (staging)");
     uint8_t* base = static_cast<uint8_t*>(staging);
     a.A = dq::NvFp4View{base, base + code_bytes, reinterpret_cast<float*>(base + code_bytes + scale_bytes), M, K};
@@ -277,7 +305,17 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
   return hip_status(e, "dq_prefill_gemm");
 }
 
-dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y, void* stream) {
+dq_status dq_decode_gemv_workspace_size(int64_t B, const dq_lut_t* W, size_t* bytes) {
+  dq_status st = check_lut(W, "W");
+  if (st != DQ_OK) return st;
+  if (B < 1 || B > 16) return fail(DQ_ERR_INVALID_ARG, "1 <= B <= 16 required");
+  if (bytes == nullptr) return fail(DQ_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = dq::gemv_workspace_bytes(B, view(W));
+  return DQ_OK;
+}
+
+dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y, void* workspace,
+                         size_t workspace_bytes, void* stream) {
   dq_status st = check_lut(W, "W");
   if (st != DQ_OK) return st;
   if (B < 1 || B > 16) return fail(DQ_ERR_INVALID_ARG, "1 <= B <= 16 required");
@@ -285,7 +323,12 @@ dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int ou
   if (out_kind != DQ_OUT_F32 && out_kind != DQ_OUT_BF16) return fail(DQ_ERR_INVALID_ARG, "bad out_kind");
   if (y == nullptr && W->rows > 0) return fail(DQ_ERR_INVALID_ARG, "y is NULL");
   if (!aligned(y, 16)) return fail(DQ_ERR_INVALID_ARG, "y must be 16-byte aligned");
-  return hip_status(dq::launch_gemv(x, B, view(W), out_kind, y, (hipStream_t)stream), "dq_decode_gemv");
+  if (workspace != nullptr) {
+    if (!aligned(workspace, 16)) return fail(DQ_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+    if (workspace_bytes < dq::gemv_workspace_bytes(B, view(W)))
+      return fail(DQ_ERR_INVALID_ARG, "workspace smaller than dq_decode_gemv_workspace_size()");
+  }
+  return hip_status(dq::launch_gemv(x, B, view(W), out_kind, y, workspace, (hipStream_t)stream), "dq_decode_gemv");
 }
 
 }  // extern "C"

@@ -51,6 +51,12 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
 // Number of compute units of the current device (queried once per device).
 int num_cus();
 
+// Stream-ordered staging from the library's memory pool on the current
+// device (created on first use; it keeps freed memory for later calls instead
+// of returning it at every free).  Release with hipFreeAsync on the same
+// stream.
+hipError_t pool_alloc_async(void** p, size_t bytes, hipStream_t s);
+
 // Column split of an M x N GEMM between workgroup tiles of bm x bn_full
 // (columns 0 .. split-1) and bm x bn_half (the rest), one workgroup per CU:
 // the split minimises the modelled time, a round of full tiles costing 1 and
@@ -74,8 +80,10 @@ inline int64_t gemm_column_split(int64_t M, int64_t N, int64_t bm, int64_t bn_fu
   return best * bn_full < N ? best * bn_full : N;
 }
 
-// a6: LUT GEMV (gemv.hip)
-hipError_t launch_gemv(const uint16_t* x, int64_t B, const LutView& w, int out_kind, void* y,
+// a6: LUT GEMV (gemv.hip).  ws: workspace of at least
+// gemv_workspace_bytes(B, w) bytes, or NULL to take it from the pool.
+size_t gemv_workspace_bytes(int64_t B, const LutView& w);
+hipError_t launch_gemv(const uint16_t* x, int64_t B, const LutView& w, int out_kind, void* y, void* ws,
                        hipStream_t s);
 
 }  // namespace dq

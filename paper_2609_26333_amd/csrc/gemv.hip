@@ -552,17 +552,8 @@ void lut_gemv_persist_kernel(const uint16_t* __restrict__ x, int B, int64_t K, c
   const _Float16* xrow = xs + (xlane ? j : 0) * rowstride + 32 * q;
   const int total = nr * CPW;
   int rd = 0, s = 0;   // consume cursor
-  const int q1 = total / 4, q2 = total / 2, q3 = (3 * total) / 4;
-  for (int f0 = 0; f0 < total; f0 += RING) {
-    if (f0 >= q3)
-      __builtin_amdgcn_s_setprio(0);
-    else if (f0 >= q2)
-      __builtin_amdgcn_s_setprio(1);
-    else if (f0 >= q1)
-      __builtin_amdgcn_s_setprio(2);
-#pragma unroll
-    for (int r = 0; r < RING; ++r) {
-      if (f0 + r >= total) break;   // past the last slot (uniform)
+  // slot r of the ring (r is a compile-time index once inlined)
+  auto slot = [&](const int r) __attribute__((always_inline)) {
       const int c = s * W + wave;
       const int xc = (rd < nr && c < KCi) ? c : KCi;   // past the end: the zero chunk
       half8_t bf[4];
@@ -602,8 +593,24 @@ void lut_gemv_persist_kernel(const uint16_t* __restrict__ x, int B, int64_t K, c
         }
         ++rd;
       }
-    }
+  };
+  // whole ring cycles without exits (an exit would make the compiler wait
+  // for every load at the top of each cycle), then the remaining slots
+  const int full = total / RING * RING;
+  const int q1 = total / 4, q2 = total / 2, q3 = (3 * total) / 4;
+  for (int f0 = 0; f0 < full; f0 += RING) {
+    if (f0 >= q3)
+      __builtin_amdgcn_s_setprio(0);
+    else if (f0 >= q2)
+      __builtin_amdgcn_s_setprio(1);
+    else if (f0 >= q1)
+      __builtin_amdgcn_s_setprio(2);
+#pragma unroll
+    for (int r = 0; r < RING; ++r) slot(r);
   }
+#pragma unroll
+  for (int r = 0; r < RING - 1; ++r)
+    if (full + r < total) slot(r);
   // ---- 5. reduce each round's W partials in order and store the tile
   __syncthreads();
   for (int r = wave; r < nr; r += W) {
@@ -633,6 +640,279 @@ void lut_gemv_persist_kernel(const uint16_t* __restrict__ x, int B, int64_t K, c
 }
 
 constexpr int kRingMulti = 8;
+
+// ---------------------------------------------------------------- batched
+// Batch B >= 2.  Each workgroup takes K group kg (KCR chunks) of a group of
+// W * TPW row tiles.  It copies the bf16 slice of x (all B rows) into LDS,
+// one wavefront per batch row rescales the row's slice by a power of two
+// from the slice's own maximum and converts it to fp16 in place (exact for
+// every value within 2^40 of that maximum), and each wavefront then owns TPW
+// whole tiles over the K group: its code stream is contiguous per tile and
+// it reduces nothing with other wavefronts.  The tile sums are unscaled per
+// batch row.  With one K group they are y; otherwise they go to a per-K-group
+// partial buffer that a reduction pass adds up in K-group order (results are
+// deterministic).  A hand-off between workgroups inside the kernel would
+// need a device-scope release per workgroup, which on this architecture
+// writes back the XCD's whole L2.
+struct SplitPlan {
+  int KG, TPW, KCR;   // K groups, tiles per wavefront, chunks per K group
+  int tiles, KC;
+};
+
+template <int BITS, int MODE, int RING, int TI>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(6)))
+void lut_gemv_split_kernel(const uint16_t* __restrict__ x, int64_t K, int B, const uint8_t* __restrict__ codes, const uint16_t* __restrict__ lut,
+                           const uint8_t* __restrict__ scales, const float* __restrict__ Gp, int64_t N,
+                           SplitPlan plan, float* __restrict__ partials, int out_kind, void* __restrict__ y) {
+  __builtin_amdgcn_s_setprio(3);
+  typedef typename CodeVec<BITS>::type cvec;
+  constexpr int kChunkBytes = 64 * CodeVec<BITS>::bytes;
+  constexpr int kTabBytes = 16 * 2 * (1 << BITS);
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int W = blockDim.x >> 6;
+  const int KG = plan.KG, TPW = plan.TPW, KCR = plan.KCR, KC = plan.KC, T = plan.tiles;
+  const int kg = (int)blockIdx.x % KG, tg = (int)blockIdx.x / KG;
+  const int tw = (tg * W + wave) * TPW;                    // this wavefront's first tile
+  const int ntw = max(0, min(TPW, T - tw));                 // and its tile count
+  const int c0 = kg * KCR, nc = min(KCR, KC - c0);         // the K group's chunks
+  const int rowstride = nc * 128 + 8;                       // fp16 per staged batch row (pad staggers banks)
+  // LDS: activations [B][rowstride] | tables [W][TI KiB] | tile sums [W][TPW][B][16] fp32;
+  // static: unscale factors and grid, copied by wavefront 0
+  __shared__ __align__(16) uint32_t s_small[32];
+  _Float16* xs = reinterpret_cast<_Float16*>(smem);
+  uint8_t* tabs = smem + round_up((int64_t)B * rowstride * 2, 16) + (size_t)wave * TI * 1024;
+  float* outs = reinterpret_cast<float*>(smem + round_up((int64_t)B * rowstride * 2, 16) + (size_t)W * TI * 1024) +
+                (size_t)wave * TPW * B * 16;
+  const int i = lane & 15, j = lane & 15, q = lane >> 4;
+  const bool xlane = j < B;
+
+  // ---- 1. the K group's slice of the raw bf16 activations (chunk-rows
+  // spread over the wavefronts; reads past K are clamped in bounds and zeroed
+  // at conversion) and this wavefront's tables
+  for (int t = wave; t < B * nc; t += W) {
+    const int b = t / nc, u = t - b * nc;
+    const int64_t k = min((int64_t)(c0 + u) * 128 + 2 * lane, K - 2);
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(x + (int64_t)b * K + k),
+                                     reinterpret_cast<void*>(xs + b * rowstride + u * 128), 4, 0, 0);
+  }
+  if (MODE == 0) {   // tables of tiles tw .. tw + TPW - 1 (contiguous); reads past the array return zero
+    const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(lut), 0, (int)((int64_t)T * kTabBytes), 0x00020000);
+#pragma unroll
+    for (int ti = 0; ti < TI; ++ti)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (__attribute__((address_space(3))) void*)(tabs + ti * 1024), 16,
+                                               lane * 16, tw * kTabBytes + ti * 1024, 0, 0);
+  }
+  // the grid into LDS as well: with only the ring's loads tracked by the
+  // compiler, its waits in the loop stay exact
+  if (MODE == 1 && wave == 0 && lane < (1 << BITS) / 2)
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(lut + 2 * lane),
+                                     reinterpret_cast<void*>(s_small + 16), 4, 0, 0);
+
+  // ---- 2. the code ring: slot (tile i, chunk u) -> chunk c0 + u of tile tw + i;
+  // past the last slot the cursor stays on it
+  const i32x4_t rcodes = buffer_resource(codes, (uint32_t)T * (uint32_t)KC * kChunkBytes);
+  i32x4_t rscales{};
+  if (MODE == 1) rscales = buffer_resource(scales, (uint32_t)T * (uint32_t)KC * 128);
+  const int32_t lane_code = lane * CodeVec<BITS>::bytes, lane_scale = lane * 2;
+  cvec ring[RING];
+  uint32_t sring[RING];
+  const int last = max(ntw, 1) - 1;   // a wavefront without tiles re-reads tile tw's range: in bounds
+  const int twc = min(tw, T - 1);
+  int li = 0, lu = 0;
+  auto load_next = [&](int slot) {
+    const int cidx = (twc + min(li, last)) * KC + c0 + lu;
+    if constexpr (BITS == 3) {
+      const i32x3_t v = raw_buffer_load_b96(rcodes, lane_code, cidx * kChunkBytes, 0);
+      ring[slot] = cvec{{(uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2]}};
+    } else {
+      const i32x2_t v = raw_buffer_load_b64(rcodes, lane_code, cidx * kChunkBytes, 0);
+      ring[slot] = cvec{{(uint32_t)v[0], (uint32_t)v[1]}};
+    }
+    if (MODE == 1) sring[slot] = (uint16_t)raw_buffer_load_b16(rscales, lane_scale, cidx * 128, 0);
+    if (++lu == nc) {
+      lu = 0;
+      ++li;
+    }
+    if (li == ntw) {
+      li = max(ntw, 1) - 1;
+      lu = nc - 1;
+    }
+  };
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int r = 0; r < RING; ++r) load_next(r);
+  __builtin_amdgcn_sched_barrier(0);
+  // the slice and table copies were issued before the ring: wait for them
+  // (the compiler does not track loads into LDS), then make every
+  // wavefront's part of the slice visible (LDS-only barrier)
+  {
+    constexpr int kv = RING * (MODE == 1 ? 2 : 1);
+    __builtin_amdgcn_s_waitcnt((kv & 0xF) | ((kv >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+  }
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  // ---- 2b. one wavefront per batch row: the slice's maximum, then fp16 in
+  // place; the row's unscale factor into LDS
+  auto to_h2 = [](uint32_t v, float sc) {
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(bf16_lo(v) * sc, bf16_hi(v) * sc));
+  };
+  for (int b = wave; b < B; b += W) {
+    uint32_t* row = reinterpret_cast<uint32_t*>(xs + b * rowstride);
+    const int nd = nc * 64;   // dwords of the slice row
+    float m = 0.0f;
+    for (int d = lane; d < nd; d += 64) {
+      const uint32_t v = row[d];
+      m = fmaxf(m, fmaxf(fabsf(bf16_lo(v)), fabsf(bf16_hi(v))));
+    }
+    const int e = stage_exponent(__float_as_uint(wave_max_dpp(m)));
+    const float sc = __builtin_ldexpf(1.0f, e);
+    for (int d = lane; d < nd; d += 64) {
+      const bool in_k = (int64_t)c0 * 128 + 2 * d < K;
+      row[d] = in_k ? to_h2(row[d], sc) : 0u;
+    }
+    if (lane == 0) s_small[b] = __float_as_uint(__builtin_ldexpf(1.0f, -e));
+  }
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  float unscale = xlane ? __uint_as_float(s_small[j]) : 1.0f;
+  if (MODE == 1) unscale *= *Gp;
+  uint4_t grid_tab{0u, 0u, 0u, 0u};
+  if (MODE == 1) {
+    if (BITS == 3)
+      grid_tab = *reinterpret_cast<const uint4_t*>(s_small + 16);
+    else
+      grid_tab = uint4_t{s_small[16], s_small[17], 0u, 0u};
+  }
+  auto tile_table = [&](int t) {
+    if (MODE == 1) return grid_tab;
+    const uint8_t* tp = tabs + t * kTabBytes + i * 2 * (1 << BITS);   // t < TI KiB / kTabBytes
+    if (BITS == 3) return *reinterpret_cast<const uint4_t*>(tp);
+    const uint2_t d = *reinterpret_cast<const uint2_t*>(tp);
+    return uint4_t{d[0], d[1], 0u, 0u};
+  };
+
+  // ---- 3. slots
+  uint32_t tl0, tl1, th0, th1;
+  table_pools<BITS>(tile_table(0), tl0, tl1, th0, th1);
+  float4_t pacc[4];
+#pragma unroll
+  for (int st = 0; st < 4; ++st) pacc[st] = float4_t{0.f, 0.f, 0.f, 0.f};
+  const _Float16* xrow = xs + (xlane ? j : 0) * rowstride + 32 * q;
+  // read the slice once before the loop: the compiler then settles its wait
+  // for the copies into LDS here, not at the top of every ring cycle
+  {
+    const uint32_t probe = *reinterpret_cast<const uint32_t*>(xrow);
+    asm volatile("" ::"v"(probe));
+  }
+  const int total = ntw * nc;
+  int ti_ = 0, u = 0;
+  auto slot = [&](const int r) __attribute__((always_inline)) {
+      half8_t bf[4];
+      const half8_t* xp = reinterpret_cast<const half8_t*>(xrow + u * 128);
+#pragma unroll
+      for (int st = 0; st < 4; ++st) bf[st] = xp[st];
+      const uint32_t sv = sring[r];
+      uint32_t sel[8];
+      selectors<BITS>(ring[r], sel);
+      load_next(r);
+      half2_t s_lo, s_hi;
+      if (MODE == 1) {
+        const half2_t sc2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sv, 1.0f, false);
+        s_lo = half2_t{sc2[0], sc2[0]};
+        s_hi = half2_t{sc2[1], sc2[1]};
+      }
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        uint32_t a0, a1, a2, a3;
+        lookup4(sel[2 * st], tl0, tl1, th0, th1, a0, a1);
+        lookup4(sel[2 * st + 1], tl0, tl1, th0, th1, a2, a3);
+        half8_t af = as_half8(a0, a1, a2, a3);
+        if (MODE == 1) af = scale_half8(af, st < 2 ? s_lo : s_hi);
+        pacc[st] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf[st], pacc[st], 0, 0, 0);
+      }
+      if (++u == nc) {   // end of tile ti_: its sums into this wavefront's LDS outputs
+        u = 0;
+        float4_t acc;
+#pragma unroll
+        for (int r2 = 0; r2 < 4; ++r2)
+          acc[r2] = ((pacc[0][r2] + pacc[1][r2]) + (pacc[2][r2] + pacc[3][r2])) * unscale;
+#pragma unroll
+        for (int st = 0; st < 4; ++st) pacc[st] = float4_t{0.f, 0.f, 0.f, 0.f};
+        if (xlane) *reinterpret_cast<float4_t*>(outs + (ti_ * B + j) * 16 + 4 * q) = acc;
+        ++ti_;
+        if (ti_ < ntw) table_pools<BITS>(tile_table(ti_), tl0, tl1, th0, th1);
+      }
+  };
+  // whole ring cycles without exits, then the remaining slots (see the
+  // batch-1 kernel); wave priority falls with progress
+  const int full = total / RING * RING;
+  const int q1 = total / 4, q2 = total / 2, q3 = (3 * total) / 4;
+  for (int f0 = 0; f0 < full; f0 += RING) {
+    if (f0 >= q3)
+      __builtin_amdgcn_s_setprio(0);
+    else if (f0 >= q2)
+      __builtin_amdgcn_s_setprio(1);
+    else if (f0 >= q1)
+      __builtin_amdgcn_s_setprio(2);
+#pragma unroll
+    for (int r = 0; r < RING; ++r) slot(r);
+  }
+#pragma unroll
+  for (int r = 0; r < RING - 1; ++r)
+    if (full + r < total) slot(r);
+  // ---- 4. store this wavefront's tile sums: y directly, or this K group's
+  // partials [KG][T][B][16]
+  const int nout = ntw * B * 16;
+  for (int e = lane; e < nout; e += 64) {
+    const int t = e / (16 * B), rem = e - t * 16 * B, jj = rem >> 4, row16 = rem & 15;
+    const int64_t row = (int64_t)(tw + t) * 16 + row16;
+    const float v = outs[e];
+    if (KG == 1) {
+      if (row < N) {
+        const int64_t o2 = (int64_t)jj * N + row;
+        if (out_kind == 0)
+          reinterpret_cast<float*>(y)[o2] = v;
+        else
+          reinterpret_cast<uint16_t*>(y)[o2] = (uint16_t)f32_to_bf16_rne(v);
+      }
+    } else {
+      partials[(((int64_t)kg * T + tw + t) * B + jj) * 16 + row16] = v;
+    }
+  }
+}
+
+// y[jj][row] = sum over the K groups, in order, of the split kernel's
+// partials [KG][T][B][16]
+__global__ __launch_bounds__(256) void reduce_partials_kernel(const float* __restrict__ partials, int KG, int T, int B,
+                                                              int64_t N, int out_kind, void* __restrict__ y) {
+  const int total = T * B * 16;
+  for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += gridDim.x * blockDim.x) {
+    const int tile = t / (B * 16);
+    const int rem = t - tile * B * 16, jj = rem >> 4, row16 = rem & 15;
+    const int64_t row = (int64_t)tile * 16 + row16;
+    if (row >= N) continue;
+    // K groups summed in order; four loads in flight per step
+    float v = 0.0f;
+    int g = 0;
+    for (; g + 4 <= KG; g += 4) {
+      const float a0 = partials[(int64_t)g * total + t], a1 = partials[(int64_t)(g + 1) * total + t];
+      const float a2 = partials[(int64_t)(g + 2) * total + t], a3 = partials[(int64_t)(g + 3) * total + t];
+      v += a0;
+      v += a1;
+      v += a2;
+      v += a3;
+    }
+    for (; g < KG; ++g) v += partials[(int64_t)g * total + t];
+    const int64_t o = (int64_t)jj * N + row;
+    if (out_kind == 0)
+      reinterpret_cast<float*>(y)[o] = v;
+    else
+      reinterpret_cast<uint16_t*>(y)[o] = (uint16_t)f32_to_bf16_rne(v);
+  }
+}
 
 // ---------------------------------------------------------------- several pieces
 template <int BITS, int MODE>
@@ -786,16 +1066,104 @@ inline int persist_wgs_per_cu(int vgprs, int waves, int64_t lds) {
   return std::max(1, std::min(by_vgpr, by_lds));
 }
 
+#ifndef DQ_GEMV_TASKS_PER_CU
+#define DQ_GEMV_TASKS_PER_CU 24
+#endif
+
+// Plan of the batch B >= 2 split-K kernel (see lut_gemv_split_kernel).
+struct BatchedPlan {
+  bool ok;               // false: the codes exceed the kernel's 32-bit offsets
+  int64_t KG, KCR, TPW;  // K groups, chunks per K group, tiles per wavefront
+  int64_t TI, G, lds;    // table KiB per wavefront, workgroups, LDS bytes
+  size_t partial_bytes;  // K-group partial sums (0 when KG == 1)
+};
+
+inline BatchedPlan plan_batched(int bits, int64_t B, int64_t T, int64_t KC) {
+  constexpr int kW = 8;
+  const int64_t tab_bytes = 32 << bits;
+  BatchedPlan p{};
+  p.ok = T * KC * 64 * (bits == 3 ? 12 : 8) < ((int64_t)1 << 31);
+  // wavefront tasks (one tile over one K group): DQ_GEMV_TASKS_PER_CU per
+  // compute unit; a K group's slice of x stays within ~40 KiB of LDS
+  const int64_t tasks = (int64_t)num_cus() * DQ_GEMV_TASKS_PER_CU;
+  const int64_t kcr_lds = std::max<int64_t>(1, (40 * 1024) / (B * 256));
+  int64_t KG = std::max<int64_t>((KC + kcr_lds - 1) / kcr_lds, std::min<int64_t>(KC, (tasks + T - 1) / T));
+  p.KCR = (KC + KG - 1) / KG;
+  p.KG = (KC + p.KCR - 1) / p.KCR;
+  p.TPW = std::min<int64_t>(16, std::max<int64_t>(1, T * p.KG / tasks));
+  p.TI = (p.TPW * tab_bytes + 1023) / 1024;
+  const int64_t TG = (T + kW * p.TPW - 1) / (kW * p.TPW);
+  p.G = p.KG * TG;
+  p.lds = round_up(B * (p.KCR * 128 + 8) * 2, 16) + kW * p.TI * 1024 + kW * p.TPW * B * 16 * 4;
+  p.partial_bytes = p.KG > 1 ? (size_t)(p.KG * T * B * 16 * 4) : 0;
+  return p;
+}
+
+// Batch B >= 2: split-K kernel, and with more than one K group a reduction
+// pass over the K-group partials, held in the caller's workspace `ws` (at
+// least plan.partial_bytes) or, when ws is NULL, in stream-ordered staging
+// from the library's pool.  Returns hipErrorNotSupported when the matrix is
+// too large for the kernel's 32-bit offsets.
 template <int BITS, int MODE>
-hipError_t launch_gemv_t(const uint16_t* x, int64_t B, const LutView& w, int out_kind, void* y, hipStream_t s) {
+hipError_t launch_gemv_batched(const uint16_t* x, int64_t B, const LutView& w, int out_kind, void* y, void* ws,
+                               hipStream_t s, int64_t T, int64_t KC) {
+  constexpr int kW = 8;
+  const int64_t N = w.rows, K = w.cols;
+  const BatchedPlan p = plan_batched(BITS, B, T, KC);
+  if (!p.ok) return hipErrorNotSupported;
+  typedef void (*kern_t)(const uint16_t*, int64_t, int, const uint8_t*, const uint16_t*, const uint8_t*,
+                         const float*, int64_t, SplitPlan, float*, int, void*);
+  kern_t kern;
+  switch (MODE == 1 ? 1 : p.TI) {
+    case 1: kern = lut_gemv_split_kernel<BITS, MODE, kRingPersist, 1>; break;
+    case 2: kern = lut_gemv_split_kernel<BITS, MODE, kRingPersist, 2>; break;
+    case 3: kern = lut_gemv_split_kernel<BITS, MODE, kRingPersist, 3>; break;
+    default: kern = lut_gemv_split_kernel<BITS, MODE, kRingPersist, 4>; break;
+  }
+  float* partials = reinterpret_cast<float*>(ws);
+  const bool pooled = p.KG > 1 && partials == nullptr;
+  hipError_t e = hipSuccess;
+  if (pooled) {
+    e = pool_alloc_async(reinterpret_cast<void**>(&partials), p.partial_bytes, s);
+    if (e != hipSuccess) return e;
+  }
+  SplitPlan sp{};
+  sp.KG = (int)p.KG;
+  sp.TPW = (int)p.TPW;
+  sp.KCR = (int)p.KCR;
+  sp.tiles = (int)T;
+  sp.KC = (int)KC;
+  hipLaunchKernelGGL(kern, dim3((unsigned)p.G), dim3(kW * 64), (size_t)p.lds, s, x, K, (int)B, w.codes, w.lut,
+                     w.scales, w.G, N, sp, partials, out_kind, y);
+  e = hipGetLastError();
+  if (p.KG > 1 && e == hipSuccess) {
+    const int64_t n = T * B * 16;
+    hipLaunchKernelGGL(reduce_partials_kernel, dim3((unsigned)std::min<int64_t>(2048, (n + 255) / 256)), dim3(256), 0,
+                       s, partials, (int)p.KG, (int)T, (int)B, N, out_kind, y);
+    e = hipGetLastError();
+  }
+  if (pooled) {
+    const hipError_t f = hipFreeAsync(partials, s);
+    if (e == hipSuccess) e = f;
+  }
+  return e;
+}
+
+template <int BITS, int MODE>
+hipError_t launch_gemv_t(const uint16_t* x, int64_t B, const LutView& w, int out_kind, void* y, void* ws,
+                         hipStream_t s) {
   const int64_t N = w.rows, K = w.cols;
   GemvPlan pl{};
   pl.tiles = round_up(N, 16) / 16;
   pl.KC = round_up(K, 128) / 128;
+  if (B >= 2) {
+    const hipError_t e = launch_gemv_batched<BITS, MODE>(x, B, w, out_kind, y, ws, s, pl.tiles, pl.KC);
+    if (e != hipErrorNotSupported) return e;
+  }
   // Persistent kernel whenever the staged activations leave room for at
   // least one workgroup per compute unit and a workgroup needs at most 8
   // rounds (2 KiB of tables per wavefront).
-  {
+  if (B == 1) {
     constexpr int kW = 8;
     constexpr int kTabBytes = 32 << BITS;
     const int64_t code_bytes = pl.tiles * pl.KC * 64 * (BITS == 3 ? 12 : 8);
@@ -886,7 +1254,13 @@ pieces:
 
 }  // namespace
 
-hipError_t launch_gemv(const uint16_t* x, int64_t B, const LutView& w, int out_kind, void* y,
+size_t gemv_workspace_bytes(int64_t B, const LutView& w) {
+  if (B < 2 || w.rows == 0 || w.cols == 0) return 0;
+  const BatchedPlan p = plan_batched(w.bits, B, round_up(w.rows, 16) / 16, round_up(w.cols, 128) / 128);
+  return p.ok ? p.partial_bytes : 0;
+}
+
+hipError_t launch_gemv(const uint16_t* x, int64_t B, const LutView& w, int out_kind, void* y, void* ws,
                        hipStream_t s) {
   if (w.rows == 0 || B == 0) return hipSuccess;
   if (w.cols == 0) {   // empty sum: y = 0 (fp32 or bf16 zeros are all-zero bits)
@@ -896,10 +1270,10 @@ hipError_t launch_gemv(const uint16_t* x, int64_t B, const LutView& w, int out_k
     return hipGetLastError();
   }
   if (w.bits == 3)
-    return w.mode == 0 ? launch_gemv_t<3, 0>(x, B, w, out_kind, y, s)
-                       : launch_gemv_t<3, 1>(x, B, w, out_kind, y, s);
-  return w.mode == 0 ? launch_gemv_t<2, 0>(x, B, w, out_kind, y, s)
-                     : launch_gemv_t<2, 1>(x, B, w, out_kind, y, s);
+    return w.mode == 0 ? launch_gemv_t<3, 0>(x, B, w, out_kind, y, ws, s)
+                       : launch_gemv_t<3, 1>(x, B, w, out_kind, y, ws, s);
+  return w.mode == 0 ? launch_gemv_t<2, 0>(x, B, w, out_kind, y, ws, s)
+                     : launch_gemv_t<2, 1>(x, B, w, out_kind, y, ws, s);
 }
 
 }  // namespace dq

@@ -28,7 +28,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert dq.abi_version() == 1
+    assert dq.abi_version() == 2
     lib = dq.lib()
     assert lib.dq_status_string(0) == b"DQ_OK"
     assert lib.dq_status_string(-1) == b"DQ_ERR_INVALID_ARG"
@@ -115,13 +115,20 @@ def test_invalid_arguments_rejected_on_host():
                                ctypes.byref(yq24), 0, None) == dq.DQ_ERR_INVALID_ARG
     # GEMV: batch out of range, bad bits
     lw = dq._Lut(fake, fake, None, None, 16, 128, 3, 0)
-    assert lib.dq_decode_gemv(fake, 0, ctypes.byref(lw), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
-    assert lib.dq_decode_gemv(fake, 17, ctypes.byref(lw), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_decode_gemv(fake, 0, ctypes.byref(lw), 0, fake, None, 0, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_decode_gemv(fake, 17, ctypes.byref(lw), 0, fake, None, 0, None) == dq.DQ_ERR_INVALID_ARG
     lw_bad = dq._Lut(fake, fake, None, None, 16, 128, 4, 0)
-    assert lib.dq_decode_gemv(fake, 1, ctypes.byref(lw_bad), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_decode_gemv(fake, 1, ctypes.byref(lw_bad), 0, fake, None, 0, None) == dq.DQ_ERR_INVALID_ARG
+    # workspace: none at B = 1, split-K partials at B >= 2; a short one is refused
+    ws = ctypes.c_size_t(123)
+    big = dq._Lut(fake, fake, None, None, 7168, 5120, 3, 0)
+    assert lib.dq_decode_gemv_workspace_size(1, ctypes.byref(big), ctypes.byref(ws)) == dq.DQ_OK and ws.value == 0
+    assert lib.dq_decode_gemv_workspace_size(16, ctypes.byref(big), ctypes.byref(ws)) == dq.DQ_OK and ws.value > 0
+    assert lib.dq_decode_gemv_workspace_size(17, ctypes.byref(big), ctypes.byref(ws)) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_decode_gemv(fake, 16, ctypes.byref(big), 0, fake, fake, ws.value - 16, None) == dq.DQ_ERR_INVALID_ARG
     # PAPER_GRID without scales / G
     lw_p = dq._Lut(fake, fake, None, None, 16, 128, 3, 1)
-    assert lib.dq_decode_gemv(fake, 1, ctypes.byref(lw_p), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_decode_gemv(fake, 1, ctypes.byref(lw_p), 0, fake, None, 0, None) == dq.DQ_ERR_INVALID_ARG
     # LUT pack: K % 32, PER_ROW K limit, bad grid
     lo = dq._Lut(fake, fake, None, None, 16, 48, 3, 0)
     assert lib.dq_pack_lut3(fake, 16, 48, 3, 0, None, ctypes.byref(lo), None) == dq.DQ_ERR_INVALID_ARG

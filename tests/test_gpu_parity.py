@@ -5,6 +5,7 @@ fp32 outputs within 1e-3 relative Frobenius error of the fp64 oracle (bf16
 outputs against the oracle rounded to bf16).  Inputs are seeded synthetic
 tensors (synth/); no expected value comes from the GPU.
 """
+import ctypes
 import os
 import sys
 
@@ -350,3 +351,27 @@ def test_gemv_large_activations_rescaled():
     y = host(dq.dq_decode_gemv(bf16_dev(xb), Wq))
     for b in range(2):
         assert linalg.rel_fro(y[b], ref[b]) <= TOL
+
+
+def test_gemv_workspace_and_pool_paths_agree():
+    """B >= 2 with split-K partials: a caller workspace and the library's own
+    pool (NULL workspace) run the same kernels and give identical outputs."""
+    N, K, B = 7168, 5120, 8
+    say("gemv workspace vs pool", N, K, B)
+    w = _lut_weight(N, K, 80)
+    Wq = dq.dq_pack_lut3(dev(w), bits=3)
+    xb = synth.random_bf16(81, (B, K), outlier_frac=0.005, outlier_factor=30)
+    x = bf16_dev(xb)
+    n = dq.dq_decode_gemv_workspace_size(B, Wq)
+    assert n > 0
+    ws = torch.full((n + 64,), 0xFF, dtype=torch.uint8, device="cuda")   # stale contents must not matter
+    y_ws = dq.dq_decode_gemv(x, Wq, workspace=ws)
+    y_ws2 = dq.dq_decode_gemv(x, Wq, workspace=ws)
+    y_pool = torch.empty_like(y_ws)
+    lib = dq.lib()
+    d = Wq.desc()
+    assert lib.dq_decode_gemv(x.data_ptr(), B, ctypes.byref(d), dq.OUT_F32, y_pool.data_ptr(), None, 0,
+                              torch.cuda.current_stream().cuda_stream) == dq.DQ_OK
+    assert torch.equal(y_ws, y_pool) and torch.equal(y_ws, y_ws2)
+    codes_ref, lut_ref = lut.quantize_per_row(w, 3)
+    assert linalg.rel_fro(host(y_ws), linalg.lut_gemv_per_row(xb, codes_ref, lut_ref)) <= TOL
