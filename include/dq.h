@@ -122,6 +122,25 @@ typedef struct dq_lut {
   int32_t mode;
 } dq_lut_t;
 
+/*
+ * MXFP4 tensor (OCP Microscaling: the W4A4 format the paper runs for models
+ * released natively in MXFP4, Sec. 4).  Logical content: rows x cols E2M1
+ * codes (as NVFP4) and one E8M0 scale code per 32 consecutive columns of a
+ * row; element value = e2m1(code) * 2^(scale - 127).  No tensor scale.
+ *
+ * Physical layout ("32x64 tiles"; R32, C64 as for NVFP4; padding elements
+ * hold code 0 and scale code 0):
+ *   codes:  as NVFP4 codes (R32*C64/2 bytes).
+ *   scales: R32*C64/32 bytes; tile (tr, tc) starts at (tr*(C64/64) + tc) * 64;
+ *           byte r + 32h is the scale of row r, columns tc*64 + 32h .. +31.
+ */
+typedef struct dq_mxfp4 {
+  uint8_t* codes;
+  uint8_t* scales;
+  int64_t rows;
+  int64_t cols;
+} dq_mxfp4_t;
+
 /* ---- diagnostics -------------------------------------------------------- */
 int dq_abi_version(void);
 const char* dq_status_string(dq_status s);
@@ -129,6 +148,10 @@ const char* dq_status_string(dq_status s);
 const char* dq_last_error(void);
 
 /* ---- size queries (host only) ------------------------------------------- */
+/* Bytes of the codes and scales buffers of a rows x cols MXFP4 tensor
+ * (cols % 32 == 0, rows >= 0). */
+dq_status dq_mxfp4_sizes(int64_t rows, int64_t cols, size_t* code_bytes, size_t* scale_bytes);
+
 /* Bytes of the codes and scales buffers of a rows x cols NVFP4 tensor
  * (cols % 16 == 0, rows >= 0). */
 dq_status dq_nvfp4_sizes(int64_t rows, int64_t cols, size_t* code_bytes, size_t* scale_bytes);
@@ -202,6 +225,24 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
                           const dq_nvfp4_t* W, int64_t M, int out_kind, void* Y,
                           const float* G_out_static, const dq_nvfp4_t* Yq, int epilogue_flags,
                           void* stream);
+
+/* ---- MXFP4 W4A4 prefill variant ------------------------------------------
+ * Quantization of a 32-block with largest magnitude a (OCP MX conversion):
+ * e = floor(log2 a) - 2, clamped to [-127, 127] (-127 for an all-zero block),
+ * scale code e + 127, codes = E2M1(x * 2^-e) nearest-even with saturation at
+ * 6, magnitude-zero codes with sign 0.
+ * dq_pack_mxfp4: W device fp32 [N, K] row-major, K % 32 == 0; out rows = N,
+ *   cols = K, buffers sized by dq_mxfp4_sizes.
+ * dq_quantize_act_mxfp4: X device bf16 [M, K]; same rule.
+ * dq_prefill_gemm_mxfp4: Y[m, n] = sum_k a_hat[m, k] * w_hat[n, k] with the
+ *   block scales applied inside the matrix cores and fp32 accumulation;
+ *   A rows = M, cols = K; W rows = N, cols = K (K = 0 gives Y = 0);
+ *   out_kind DQ_OUT_F32 / DQ_OUT_BF16, Y device [M, N] row-major. */
+dq_status dq_pack_mxfp4(const float* W, int64_t N, int64_t K, const dq_mxfp4_t* out, void* stream);
+dq_status dq_quantize_act_mxfp4(const uint16_t* X, int64_t M, int64_t K, const dq_mxfp4_t* out,
+                                void* stream);
+dq_status dq_prefill_gemm_mxfp4(const dq_mxfp4_t* A, const dq_mxfp4_t* W, int out_kind, void* Y,
+                                void* stream);
 
 /* ---- a6: weight-only LUT GEMV (decode; no activation quantization) -------
  * The weight-only path the paper serves decode with (Sec. 3 "Format

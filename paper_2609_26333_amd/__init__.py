@@ -39,6 +39,11 @@ class _NvFp4(ctypes.Structure):
                 ("rows", ctypes.c_int64), ("cols", ctypes.c_int64)]
 
 
+class _MxFp4(ctypes.Structure):
+    _fields_ = [("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p), ("rows", ctypes.c_int64),
+                ("cols", ctypes.c_int64)]
+
+
 class _Lut(ctypes.Structure):
     _fields_ = [("codes", ctypes.c_void_p), ("lut", ctypes.c_void_p), ("scales", ctypes.c_void_p),
                 ("G", ctypes.c_void_p), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
@@ -62,6 +67,10 @@ def _load() -> ctypes.CDLL:
         "dq_quantize_act_nvfp4": (S, [P, I64, I64, P, ctypes.POINTER(_NvFp4), P]),
         "dq_prefill_gemm": (S, [ctypes.POINTER(_NvFp4), P, P, ctypes.POINTER(_NvFp4), I64, I32, P, P,
                                 ctypes.POINTER(_NvFp4), I32, P]),
+        "dq_mxfp4_sizes": (S, [I64, I64, SZ, SZ]),
+        "dq_pack_mxfp4": (S, [P, I64, I64, ctypes.POINTER(_MxFp4), P]),
+        "dq_quantize_act_mxfp4": (S, [P, I64, I64, ctypes.POINTER(_MxFp4), P]),
+        "dq_prefill_gemm_mxfp4": (S, [ctypes.POINTER(_MxFp4), ctypes.POINTER(_MxFp4), I32, P, P]),
         "dq_decode_gemv_workspace_size": (S, [I64, ctypes.POINTER(_Lut), SZ]),
         "dq_decode_gemv": (S, [P, I64, ctypes.POINTER(_Lut), I32, P, P, ctypes.c_size_t, P]),
     }
@@ -75,7 +84,8 @@ def _load() -> ctypes.CDLL:
 _lib = _load()
 EXPORTED = ("dq_abi_version", "dq_status_string", "dq_last_error", "dq_nvfp4_sizes", "dq_lut_sizes",
             "dq_pack_nvfp4", "dq_pack_lut3", "dq_quantize_act_nvfp4", "dq_prefill_gemm",
-            "dq_decode_gemv_workspace_size", "dq_decode_gemv")
+            "dq_decode_gemv_workspace_size", "dq_decode_gemv", "dq_mxfp4_sizes", "dq_pack_mxfp4",
+            "dq_quantize_act_mxfp4", "dq_prefill_gemm_mxfp4")
 
 
 def lib() -> ctypes.CDLL:
@@ -107,6 +117,12 @@ def nvfp4_sizes(rows: int, cols: int):
     return c.value, s.value
 
 
+def mxfp4_sizes(rows: int, cols: int):
+    c, s = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(_lib.dq_mxfp4_sizes(rows, cols, ctypes.byref(c), ctypes.byref(s)), "dq_mxfp4_sizes")
+    return c.value, s.value
+
+
 def lut_sizes(bits: int, mode: int, rows: int, cols: int):
     c, l, s = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
     _check(_lib.dq_lut_sizes(bits, mode, rows, cols, ctypes.byref(c), ctypes.byref(l), ctypes.byref(s)),
@@ -133,6 +149,24 @@ class NvFp4Tensor:
 
     def desc(self) -> _NvFp4:
         return _NvFp4(self.codes.data_ptr(), self.scales.data_ptr(), self.G.data_ptr(), self.rows, self.cols)
+
+
+@dataclasses.dataclass
+class MxFp4Tensor:
+    """MXFP4 tensor in the tiled device layout of dq.h (uint8 codes and E8M0 scales)."""
+    codes: torch.Tensor
+    scales: torch.Tensor
+    rows: int
+    cols: int
+
+    @staticmethod
+    def empty(rows: int, cols: int, device="cuda") -> "MxFp4Tensor":
+        cb, sb = mxfp4_sizes(rows, cols)
+        return MxFp4Tensor(torch.empty(max(cb, 16), dtype=torch.uint8, device=device),
+                           torch.empty(max(sb, 16), dtype=torch.uint8, device=device), rows, cols)
+
+    def desc(self) -> _MxFp4:
+        return _MxFp4(self.codes.data_ptr(), self.scales.data_ptr(), self.rows, self.cols)
 
 
 @dataclasses.dataclass
@@ -237,6 +271,37 @@ def dq_prefill_gemm(W: NvFp4Tensor, A: Optional[NvFp4Tensor] = None, X: Optional
     return Yq if out_kind == OUT_NVFP4 else Y
 
 
+def dq_pack_mxfp4(W: torch.Tensor, out: Optional[MxFp4Tensor] = None, stream=None) -> MxFp4Tensor:
+    assert W.dtype == torch.float32 and W.is_contiguous() and W.dim() == 2
+    N, K = W.shape
+    out = MxFp4Tensor.empty(N, K, W.device) if out is None else out
+    d = out.desc()
+    _check(_lib.dq_pack_mxfp4(W.data_ptr(), N, K, ctypes.byref(d), _stream(stream)), "dq_pack_mxfp4")
+    return out
+
+
+def dq_quantize_act_mxfp4(X: torch.Tensor, out: Optional[MxFp4Tensor] = None, stream=None) -> MxFp4Tensor:
+    X = _as_u16(X)
+    assert X.is_contiguous() and X.dim() == 2
+    M, K = X.shape
+    out = MxFp4Tensor.empty(M, K, X.device) if out is None else out
+    d = out.desc()
+    _check(_lib.dq_quantize_act_mxfp4(X.data_ptr(), M, K, ctypes.byref(d), _stream(stream)),
+           "dq_quantize_act_mxfp4")
+    return out
+
+
+def dq_prefill_gemm_mxfp4(A: MxFp4Tensor, W: MxFp4Tensor, out_kind: int = OUT_F32,
+                          Y: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    if Y is None:
+        Y = torch.empty((A.rows, W.rows), dtype=torch.float32 if out_kind == OUT_F32 else torch.bfloat16,
+                        device=W.codes.device)
+    da, dw = A.desc(), W.desc()
+    _check(_lib.dq_prefill_gemm_mxfp4(ctypes.byref(da), ctypes.byref(dw), out_kind, Y.data_ptr(), _stream(stream)),
+           "dq_prefill_gemm_mxfp4")
+    return Y
+
+
 _gemv_ws_cache: dict = {}
 
 
@@ -274,4 +339,4 @@ def dq_decode_gemv(x: torch.Tensor, W: LutWeight, out_kind: int = OUT_F32, y: Op
 
 
 __all__ = [n for n in dir() if n.startswith(("dq_", "DQ", "OUT_", "LUT_", "EPI_")) or n in
-           ("NvFp4Tensor", "LutWeight", "nvfp4_sizes", "lut_sizes", "abi_version", "lib", "EXPORTED")]
+           ("NvFp4Tensor", "MxFp4Tensor", "LutWeight", "nvfp4_sizes", "mxfp4_sizes", "lut_sizes", "abi_version", "lib", "EXPORTED")]

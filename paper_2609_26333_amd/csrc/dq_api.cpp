@@ -53,6 +53,22 @@ dq_status check_nvfp4(const dq_nvfp4_t* t, const char* name, int64_t rows, int64
 
 dq::NvFp4View view(const dq_nvfp4_t* t) { return dq::NvFp4View{t->codes, t->scales, t->G, t->rows, t->cols}; }
 
+dq_status check_mxfp4(const dq_mxfp4_t* t, const char* name, int64_t rows, int64_t cols) {
+  if (t == nullptr) return fail(DQ_ERR_INVALID_ARG, "%s is NULL", name);
+  if (t->rows < 0 || t->cols < 0 || t->cols % 32 != 0)
+    return fail(DQ_ERR_INVALID_ARG, "%s: rows >= 0 and cols %% 32 == 0 required", name);
+  if (rows >= 0 && (t->rows != rows || t->cols != cols))
+    return fail(DQ_ERR_INVALID_ARG, "%s is %lldx%lld, expected %lldx%lld", name, (long long)t->rows,
+                (long long)t->cols, (long long)rows, (long long)cols);
+  if (t->rows * t->cols > 0 && (t->codes == nullptr || t->scales == nullptr))
+    return fail(DQ_ERR_INVALID_ARG, "%s has a NULL buffer", name);
+  if (!aligned(t->codes, 16) || !aligned(t->scales, 16))
+    return fail(DQ_ERR_INVALID_ARG, "%s buffers must be 16-byte aligned", name);
+  return DQ_OK;
+}
+
+dq::MxView view(const dq_mxfp4_t* t) { return dq::MxView{t->codes, t->scales, t->rows, t->cols}; }
+
 dq_status check_lut(const dq_lut_t* t, const char* name) {
   if (t == nullptr) return fail(DQ_ERR_INVALID_ARG, "%s is NULL", name);
   if (t->bits != 2 && t->bits != 3) return fail(DQ_ERR_INVALID_ARG, "%s.bits must be 2 or 3", name);
@@ -149,6 +165,16 @@ dq_status dq_nvfp4_sizes(int64_t rows, int64_t cols, size_t* code_bytes, size_t*
   const int64_t r = rup(rows, 32), c = rup(cols, 64);
   *code_bytes = (size_t)(r * c / 2);
   *scale_bytes = (size_t)(r * c / 16);
+  return ok();
+}
+
+dq_status dq_mxfp4_sizes(int64_t rows, int64_t cols, size_t* code_bytes, size_t* scale_bytes) {
+  if (code_bytes == nullptr || scale_bytes == nullptr) return fail(DQ_ERR_INVALID_ARG, "NULL output pointer");
+  if (rows < 0 || cols < 0 || cols % 32 != 0)
+    return fail(DQ_ERR_INVALID_ARG, "rows >= 0, cols >= 0 and cols %% 32 == 0 required");
+  const int64_t r = rup(rows, 32), c = rup(cols, 64);
+  *code_bytes = (size_t)(r * c / 2);
+  *scale_bytes = (size_t)(r * c / 32);
   return ok();
 }
 
@@ -303,6 +329,44 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
     if (e == hipSuccess) e = f;
   }
   return hip_status(e, "dq_prefill_gemm");
+}
+
+dq_status dq_pack_mxfp4(const float* W, int64_t N, int64_t K, const dq_mxfp4_t* out, void* stream) {
+  if (W == nullptr && N * K > 0) return fail(DQ_ERR_INVALID_ARG, "W is NULL");
+  if (!aligned(W, 16)) return fail(DQ_ERR_INVALID_ARG, "W must be 16-byte aligned");
+  if (N < 0 || K < 0 || K % 32 != 0) return fail(DQ_ERR_INVALID_ARG, "N >= 0, K >= 0, K %% 32 == 0 required");
+  dq_status st = check_mxfp4(out, "out", N, K);
+  if (st != DQ_OK) return st;
+  return hip_status(dq::launch_mx_quantize(W, false, N, K, view(out), (hipStream_t)stream), "dq_pack_mxfp4");
+}
+
+dq_status dq_quantize_act_mxfp4(const uint16_t* X, int64_t M, int64_t K, const dq_mxfp4_t* out, void* stream) {
+  if (X == nullptr && M * K > 0) return fail(DQ_ERR_INVALID_ARG, "X is NULL");
+  if (!aligned(X, 16)) return fail(DQ_ERR_INVALID_ARG, "X must be 16-byte aligned");
+  if (M < 0 || K < 0 || K % 32 != 0) return fail(DQ_ERR_INVALID_ARG, "M >= 0, K >= 0, K %% 32 == 0 required");
+  dq_status st = check_mxfp4(out, "out", M, K);
+  if (st != DQ_OK) return st;
+  return hip_status(dq::launch_mx_quantize(X, true, M, K, view(out), (hipStream_t)stream), "dq_quantize_act_mxfp4");
+}
+
+dq_status dq_prefill_gemm_mxfp4(const dq_mxfp4_t* A, const dq_mxfp4_t* W, int out_kind, void* Y, void* stream) {
+  dq_status st = check_mxfp4(W, "W", -1, -1);
+  if (st != DQ_OK) return st;
+  if (A == nullptr) return fail(DQ_ERR_INVALID_ARG, "A is NULL");
+  st = check_mxfp4(A, "A", A->rows, W->cols);
+  if (st != DQ_OK) return st;
+  if (out_kind != DQ_OUT_F32 && out_kind != DQ_OUT_BF16) return fail(DQ_ERR_INVALID_ARG, "bad out_kind");
+  if (Y == nullptr && A->rows * W->rows > 0) return fail(DQ_ERR_INVALID_ARG, "Y is NULL");
+  if (!aligned(Y, 16)) return fail(DQ_ERR_INVALID_ARG, "Y must be 16-byte aligned");
+  dq::MxGemmArgs a{};
+  a.A = view(A);
+  a.W = view(W);
+  a.M = A->rows;
+  a.N = W->rows;
+  a.K = W->cols;
+  a.out_kind = out_kind;
+  a.Y = Y;
+  return hip_status(dq::launch_mx_gemm(a, (hipStream_t)stream), "dq_prefill_gemm_mxfp4");
 }
 
 dq_status dq_decode_gemv_workspace_size(int64_t B, const dq_lut_t* W, size_t* bytes) {

@@ -48,6 +48,23 @@ struct GemmArgs {
 };
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
 
+// MXFP4 (mxfp4.hip): codes and E8M0 scales in the 32x64-tile layout of dq.h
+struct MxView {
+  uint8_t* codes;
+  uint8_t* scales;
+  int64_t rows, cols;
+};
+// x: bf16 bits (is_bf16) or fp32, [rows, cols] row-major
+hipError_t launch_mx_quantize(const void* x, bool is_bf16, int64_t rows, int64_t cols, const MxView& out,
+                              hipStream_t s);
+struct MxGemmArgs {
+  MxView A, W;
+  int64_t M, N, K;
+  int out_kind;   // 0 fp32, 1 bf16
+  void* Y;
+};
+hipError_t launch_mx_gemm(const MxGemmArgs& a, hipStream_t s);
+
 // Number of compute units of the current device (queried once per device).
 int num_cus();
 

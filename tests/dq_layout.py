@@ -43,6 +43,37 @@ def nvfp4_pack(codes: np.ndarray, scale_codes: np.ndarray):
     return cb, sb
 
 
+# ---------------------------------------------------------------- MXFP4
+def mxfp4_unpack(codes: np.ndarray, scales: np.ndarray, rows: int, cols: int):
+    """Tiled MXFP4 buffers -> logical codes [rows, cols] and scale codes [rows, cols/32]
+    (plus the padded arrays)."""
+    R, C = _ru(rows, 32), _ru(cols, 64)
+    tr, tc = R // 32, C // 64
+    cb = np.asarray(codes, np.uint8)[: R * C // 2].reshape(tr, tc, 32, 32)
+    q = np.empty((tr, tc, 32, 64), np.uint8)
+    q[..., 0::2] = cb & 0xF
+    q[..., 1::2] = cb >> 4
+    q = q.transpose(0, 2, 1, 3).reshape(R, C)
+    # tile scale byte r + 32h = row r, 32-block h of the tile
+    sb = np.asarray(scales, np.uint8)[: R * C // 32].reshape(tr, tc, 2, 32).transpose(0, 3, 1, 2).reshape(R, C // 32)
+    return q[:rows, :cols], sb[:rows, : cols // 32], q, sb
+
+
+def mxfp4_pack(codes: np.ndarray, scale_codes: np.ndarray):
+    """Logical codes [rows, cols] and scale codes [rows, cols/32] -> tiled buffers."""
+    rows, cols = codes.shape
+    R, C = _ru(rows, 32), _ru(cols, 64)
+    q = np.zeros((R, C), np.uint8)
+    q[:rows, :cols] = codes
+    s = np.zeros((R, C // 32), np.uint8)
+    s[:rows, : cols // 32] = scale_codes
+    tr, tc = R // 32, C // 64
+    qt = q.reshape(tr, 32, tc, 64).transpose(0, 2, 1, 3)
+    cb = (qt[..., 0::2] | (qt[..., 1::2] << 4)).astype(np.uint8).reshape(-1)
+    sb = s.reshape(tr, 32, tc, 2).transpose(0, 2, 3, 1).reshape(-1).astype(np.uint8)
+    return cb, sb
+
+
 # ---------------------------------------------------------------- LUT
 def _code_positions(bits):
     """For t in 0..31: list of (dword, shift, width, value_shift) pieces."""

@@ -48,6 +48,29 @@ def test_size_queries():
         dq.lut_sizes(4, 0, 16, 32)
     with pytest.raises(dq.DQError):
         dq.lut_sizes(3, 0, 16, 48)
+    assert dq.mxfp4_sizes(100, 96) == (128 * 128 // 2, 128 * 128 // 32)
+    assert dq.mxfp4_sizes(0, 0) == (0, 0)
+    with pytest.raises(dq.DQError):
+        dq.mxfp4_sizes(4, 48)
+
+
+def test_mxfp4_arguments_rejected_on_host():
+    lib = dq.lib()
+    fake = 1 << 20
+    mx = lambda r, c, codes=fake, scales=fake: dq._MxFp4(codes, scales, r, c)   # noqa: E731
+    P = ctypes.byref
+    # K % 32, descriptor shape, NULL / misaligned buffers
+    assert lib.dq_pack_mxfp4(fake, 4, 48, P(mx(4, 48)), None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_pack_mxfp4(fake, 4, 64, P(mx(4, 32)), None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_pack_mxfp4(fake, 4, 64, P(mx(4, 64, codes=None)), None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_pack_mxfp4(fake + 4, 4, 64, P(mx(4, 64)), None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_quantize_act_mxfp4(fake, 4, 64, P(mx(4, 64, scales=fake + 8)), None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_quantize_act_mxfp4(None, 4, 64, P(mx(4, 64)), None) == dq.DQ_ERR_INVALID_ARG
+    # GEMM: K mismatch, bad out_kind, NULL Y
+    assert lib.dq_prefill_gemm_mxfp4(P(mx(4, 64)), P(mx(8, 128)), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_prefill_gemm_mxfp4(P(mx(4, 64)), P(mx(8, 64)), dq.OUT_NVFP4, fake, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_prefill_gemm_mxfp4(P(mx(4, 64)), P(mx(8, 64)), 0, None, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_prefill_gemm_mxfp4(None, P(mx(8, 64)), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
 
 
 def _nv(rows, cols, codes=16, scales=16, G=16):
