@@ -128,11 +128,13 @@ typedef struct dq_lut {
  * codes (as NVFP4) and one E8M0 scale code per 32 consecutive columns of a
  * row; element value = e2m1(code) * 2^(scale - 127).  No tensor scale.
  *
- * Physical layout ("32x64 tiles"; R32, C64 as for NVFP4; padding elements
- * hold code 0 and scale code 0):
+ * Physical layout ("32x64 tiles"; R32, C64 as for NVFP4, R128 = rows rounded
+ * up to 128; padding elements hold code 0 and scale code 0):
  *   codes:  as NVFP4 codes (R32*C64/2 bytes).
- *   scales: R32*C64/32 bytes; tile (tr, tc) starts at (tr*(C64/64) + tc) * 64;
- *           byte r + 32h is the scale of row r, columns tc*64 + 32h .. +31.
+ *   scales: R128*C64/32 bytes in groups of 4 row tiles: group (g, tc) (rows
+ *           128g .. 128g+127, columns tc*64 .. +63) starts at
+ *           (g*(C64/64) + tc) * 256; byte 4*(r + 32h) + q is the scale of row
+ *           128g + 32q + r, columns tc*64 + 32h .. +31.
  */
 typedef struct dq_mxfp4 {
   uint8_t* codes;

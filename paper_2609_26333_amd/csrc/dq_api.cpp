@@ -172,9 +172,9 @@ dq_status dq_mxfp4_sizes(int64_t rows, int64_t cols, size_t* code_bytes, size_t*
   if (code_bytes == nullptr || scale_bytes == nullptr) return fail(DQ_ERR_INVALID_ARG, "NULL output pointer");
   if (rows < 0 || cols < 0 || cols % 32 != 0)
     return fail(DQ_ERR_INVALID_ARG, "rows >= 0, cols >= 0 and cols %% 32 == 0 required");
-  const int64_t r = rup(rows, 32), c = rup(cols, 64);
-  *code_bytes = (size_t)(r * c / 2);
-  *scale_bytes = (size_t)(r * c / 32);
+  const int64_t c = rup(cols, 64);
+  *code_bytes = (size_t)(rup(rows, 32) * c / 2);
+  *scale_bytes = (size_t)(rup(rows, 128) * c / 32);
   return ok();
 }
 

@@ -31,8 +31,8 @@
 //    steps ahead of the consumer, one workgroup barrier per K step;
 //  * the operands of K step kt+1 are read from LDS into registers while the
 //    MFMAs of step kt run;
-//  * workgroups are numbered so that the 8 XCDs each own a contiguous range
-//    of output tiles (column-panel-major).
+//  * output tiles are handed out in bands of row panels, with each XCD taking
+//    a compact sub-block of the tiles in flight (see tile_of).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -55,11 +55,13 @@ __device__ inline int floor_log2(float a) {
 }
 
 // ---------------------------------------------------------------- quantizer
-// One wavefront per 32x64 tile: lane l = row l%32, columns 32*(l/32)..+31 of
-// the tile (one MX block).  Codes: the lane's 16 bytes at 32*(l%32) +
-// 16*(l/32) of the tile (row-major 32 bytes per row); scales: byte l of the
-// tile's 64.  Rows past `rows` and columns past `cols` produce zero codes and
-// scale code 0.
+// One workgroup per 4-tile scale group: wavefront q quantizes the 32x64 tile
+// (4g + q, tc); lane l = row l%32, columns 32*(l/32)..+31 of the tile (one
+// MX block).  Codes: the lane's 16 bytes at 32*(l%32) + 16*(l/32) of the tile
+// (row-major 32 bytes per row).  Scales: byte 4l + q of the group's 256, so
+// that one dword per lane carries the scales of 4 row tiles (the GEMM's
+// operand).  Rows past `rows` and columns past `cols` produce zero codes and
+// scale code 0; tiles past the last row tile (group padding) get scale 0 only.
 template <typename T>
 __device__ inline void load_block(const T* __restrict__ src, float (&v)[32]);
 
@@ -92,10 +94,10 @@ template <typename T>
 __global__ __launch_bounds__(256) void mx_quantize_kernel(const T* __restrict__ x, int64_t rows, int64_t cols,
                                                           int64_t tiles_r, int64_t tiles_c,
                                                           uint8_t* __restrict__ codes, uint8_t* __restrict__ scales) {
-  const int lane = threadIdx.x & 63;
-  const int64_t tile = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (tile >= tiles_r * tiles_c) return;
-  const int64_t tr = tile / tiles_c, tc = tile - tr * tiles_c;
+  __shared__ uint32_t s_grp[64];
+  const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int64_t g = blockIdx.x / tiles_c, tc = blockIdx.x - g * tiles_c;
+  const int64_t tr = 4 * g + q;
   const int r = lane & 31, h = lane >> 5;
   const int64_t row = tr * 32 + r, col = tc * 64 + h * 32;
   float v[32];
@@ -113,18 +115,22 @@ __global__ __launch_bounds__(256) void mx_quantize_kernel(const T* __restrict__ 
   // 2^-e as fp32: -e lies in [-125, 127] for finite inputs (a < 2^128 gives
   // e <= 125), so the biased exponent 127 - e is in [2, 254]
   const float p = __uint_as_float((uint32_t)(127 - e) << 23);
-  uint4_t out;
+  if (tr < tiles_r) {
+    uint4_t out;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    uint32_t w = 0u;
-    w = cvt_pk_fp4<0>(w, v[8 * q] * p, v[8 * q + 1] * p);
-    w = cvt_pk_fp4<1>(w, v[8 * q + 2] * p, v[8 * q + 3] * p);
-    w = cvt_pk_fp4<2>(w, v[8 * q + 4] * p, v[8 * q + 5] * p);
-    w = cvt_pk_fp4<3>(w, v[8 * q + 6] * p, v[8 * q + 7] * p);
-    out[q] = fp4_canonical_zero(w);
+    for (int k = 0; k < 4; ++k) {
+      uint32_t w = 0u;
+      w = cvt_pk_fp4<0>(w, v[8 * k] * p, v[8 * k + 1] * p);
+      w = cvt_pk_fp4<1>(w, v[8 * k + 2] * p, v[8 * k + 3] * p);
+      w = cvt_pk_fp4<2>(w, v[8 * k + 4] * p, v[8 * k + 5] * p);
+      w = cvt_pk_fp4<3>(w, v[8 * k + 6] * p, v[8 * k + 7] * p);
+      out[k] = fp4_canonical_zero(w);
+    }
+    *reinterpret_cast<uint4_t*>(codes + (tr * tiles_c + tc) * 1024 + r * 32 + h * 16) = out;
   }
-  *reinterpret_cast<uint4_t*>(codes + tile * 1024 + r * 32 + h * 16) = out;
-  scales[tile * 64 + lane] = (uint8_t)(e + 127);
+  reinterpret_cast<uint8_t*>(s_grp)[4 * lane + q] = (uint8_t)(e + 127);
+  __syncthreads();
+  if (q == 0) reinterpret_cast<uint32_t*>(scales + (g * tiles_c + tc) * 256)[lane] = s_grp[lane];
 }
 
 // ---------------------------------------------------------------- GEMM
@@ -142,15 +148,15 @@ struct MxGeo {
   // one stage = one 64-column K step: A codes, W codes, A scales, W scales
   static constexpr int a_codes = 0;
   static constexpr int w_codes = at * 1024;
-  static constexpr int a_scales = w_codes + wt * 1024;
+  static constexpr int a_scales = w_codes + wt * 1024;   // 4-tile scale groups of 256 bytes
   static constexpr int w_scales = a_scales + at * 64;
   static constexpr int bytes = w_scales + wt * 64;
   static constexpr int stages_fit = kMxLdsBudget / bytes;
   static constexpr int stages = stages_fit < 6 ? stages_fit : 6;
-  // direct loads per stage: one per code tile; one dword load covers 4 scale tiles
+  // direct loads per stage: one per code tile; one dword load per 4-tile scale group
   static constexpr int code_loads = at + wt;
   static constexpr int scale_loads = (at + wt) / 4;
-  static_assert((at + wt) % 4 == 0 && at % 4 == 0, "scale tiles are loaded four at a time");
+  static_assert(wt % 4 == 0 && at % 4 == 0, "scale groups of 4 tiles");
   static_assert(code_loads % waves == 0 && scale_loads <= waves, "uniform load distribution");
   static constexpr int loads_per_wave = code_loads / waves + 1;   // + one scale load (some waves: a dummy)
   static_assert(stages >= 4, "LDS ring needs four stages");
@@ -167,6 +173,30 @@ __device__ inline void mx_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Output tile of workgroup b.  Tiles are ordered in bands of GM row panels,
+// row panel fastest within a band, so that the ~256 workgroups in flight at
+// once cover about GM x 256/GM tiles and share their A and W panels through
+// the L2 and the MALL.  Workgroup b runs on XCD b % 8; within each complete
+// group of 256 workgroups the 32 of one XCD take a 4 x 8 sub-block, so each
+// XCD's L2 streams 12 panels instead of up to 33.
+__device__ inline void tile_of(int64_t b, int64_t tiles_m, int64_t tiles_n, int64_t& bm, int64_t& bn) {
+  const int64_t nb = tiles_m * tiles_n;
+  const int GM = tiles_m >= 16 ? 16 : tiles_m >= 8 ? 8 : tiles_m >= 4 ? 4 : (int)tiles_m;
+  int64_t L = b;
+  if ((GM == 4 || GM == 8 || GM == 16) && (b | 255) < nb) {
+    const int q = (int)(b & 255), xcd = q & 7, loc = q >> 3;
+    const int xm = GM / 4;
+    const int m_in = (xcd % xm) * 4 + (loc & 3), n_in = (xcd / xm) * 8 + (loc >> 2);
+    L = b - q + m_in + GM * n_in;
+  }
+  const int64_t band = L / (GM * tiles_n);
+  const int64_t first = band * GM;
+  const int64_t gm = tiles_m - first < GM ? tiles_m - first : GM;
+  const int64_t idx = L - band * GM * tiles_n;
+  bm = first + idx % gm;
+  bn = idx / gm;
+}
+
 template <class Gm, int OUT>
 __global__ __launch_bounds__(Gm::threads, 1) void mxfp4_gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales, const uint8_t* __restrict__ w_codes,
@@ -179,10 +209,8 @@ __global__ __launch_bounds__(Gm::threads, 1) void mxfp4_gemm_kernel(
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int64_t nb = tiles_m * tiles_n;
-  int64_t logical = blockIdx.x;
-  if (nb % 8 == 0) logical = (int64_t)(blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8;
-  const int64_t bm = logical % tiles_m, bn = logical / tiles_m;
+  int64_t bm, bn;
+  tile_of(blockIdx.x, tiles_m, tiles_n, bm, bn);
   const int wm = wave % Gm::wm, wn = wave / Gm::wm;
   const int64_t a_tr0 = bm * Gm::at, w_tr0 = n_off / 32 + bn * Gm::wt;
   const int64_t m0 = bm * Gm::bm + wm * 32 * TM;
@@ -190,9 +218,11 @@ __global__ __launch_bounds__(Gm::threads, 1) void mxfp4_gemm_kernel(
   const int KTi = (int)KT;
 
   // Direct loads: code tiles t = wave + waves*u (A tiles first, then W);
-  // scale instruction `wave` covers 4 tiles (16 lanes each).  Tiles past the
-  // end of an operand read its last row tile (in bounds): they only feed
-  // output rows / columns that are never stored.
+  // scale instruction `wave` covers one 4-tile group (256 bytes).  Tiles past
+  // the end of an operand read its last row tile (in bounds): they only feed
+  // output rows / columns that are never stored.  K steps past the end
+  // reload the last one into a slot that is no longer read, so that every
+  // step issues the same loads (no branches in the main loop).
   const int chunk = 2 * (lane & 31) + (lane >> 5);
   constexpr int CPW = Gm::code_loads / Gm::waves;
   const uint8_t* c_src[CPW];
@@ -206,20 +236,21 @@ __global__ __launch_bounds__(Gm::threads, 1) void mxfp4_gemm_kernel(
     c_src[u] = (is_a ? a_codes : w_codes) + tr * KT * 1024 + chunk * 16;
     c_dst[u] = (is_a ? Gm::a_codes : Gm::w_codes) + b * 1024;
   }
-  const int st = min(wave, Gm::scale_loads - 1) * 4 + (lane >> 4);   // scale tile of this lane
-  const bool s_is_a = st < Gm::at;
-  const int sb = s_is_a ? st : st - Gm::at;
-  const int64_t s_tr = min((s_is_a ? a_tr0 : w_tr0) + sb, (s_is_a ? a_tiles_r : w_tiles_r) - 1);
-  const uint8_t* s_src = (s_is_a ? a_scales : w_scales) + s_tr * KT * 64 + (lane & 15) * 4;
-  // waves past the scale instructions repeat the last one (same bytes, same place)
-  const int s_dst = (Gm::a_scales + (min(wave, Gm::scale_loads - 1) * 4) * 64);
+  const int si = min(wave, Gm::scale_loads - 1);   // waves past the last scale group repeat it
+  const bool s_is_a = si < Gm::at / 4;
+  const int64_t a_groups = (a_tiles_r + 3) / 4, w_groups = (w_tiles_r + 3) / 4;
+  const int64_t sg = min((s_is_a ? a_tr0 : w_tr0) / 4 + (s_is_a ? si : si - Gm::at / 4),
+                         (s_is_a ? a_groups : w_groups) - 1);
+  const uint8_t* s_src = (s_is_a ? a_scales : w_scales) + sg * KT * 256 + lane * 4;
+  const int s_dst = Gm::a_scales + si * 256;
   auto issue = [&](int kt) {
     uint8_t* stage = smem + (kt % S) * Gm::bytes;
+    const int ktc = kt < KTi ? kt : KTi - 1;
 #pragma unroll
     for (int u = 0; u < CPW; ++u)
-      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(c_src[u] + (size_t)kt * 1024),
+      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(c_src[u] + (size_t)ktc * 1024),
                                        reinterpret_cast<void*>(stage + c_dst[u]), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(s_src + (size_t)kt * 64),
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(s_src + (size_t)ktc * 256),
                                      reinterpret_cast<void*>(stage + s_dst), 4, 0, 0);
   };
 
@@ -229,101 +260,153 @@ __global__ __launch_bounds__(Gm::threads, 1) void mxfp4_gemm_kernel(
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = float16_t{};
 
+  // Operands of one K step: code tiles, and the scale bytes of the
+  // wavefront's A tiles (byte i = tile i) and W tiles (byte j = tile j) in
+  // one dword each.
   struct Ops {
     uint4_t a[TM], w[TN];
-    uint32_t sa[TM], sw[TN];
+    uint32_t sa, sw;
   };
+  static_assert(TM == 4 && (TN == 4 || TN == 2), "scale dwords hold 4 tiles");
   const int a_rd = Gm::a_codes + wm * TM * 1024 + lane * 16;
   const int w_rd = Gm::w_codes + wn * TN * 1024 + lane * 16;
-  const int as_rd = Gm::a_scales + wm * TM * 64 + lane;
-  const int ws_rd = Gm::w_scales + wn * TN * 64 + lane;
-  auto read_ops = [&](int kt, Ops& o) {
-    const uint8_t* stg = smem + (kt % S) * Gm::bytes;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      o.a[i] = *reinterpret_cast<const uint4_t*>(stg + a_rd + i * 1024);
-      o.sa[i] = stg[as_rd + i * 64];
-    }
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      o.w[j] = *reinterpret_cast<const uint4_t*>(stg + w_rd + j * 1024);
-      o.sw[j] = stg[ws_rd + j * 64];
+  const int as_rd = Gm::a_scales + wm * 256 + lane * 4;
+  const int ws_rd = Gm::w_scales + (wn * TN / 4) * 256 + lane * 4;
+  const int ws_shift = 8 * ((wn * TN) % 4);
+  // read r (0 .. TM+TN+1) of a step's operands
+  auto read_one = [&](const uint8_t* stg, Ops& o, int r) {
+    if (r < TM) o.a[r] = *reinterpret_cast<const uint4_t*>(stg + a_rd + r * 1024);
+    else if (r < TM + TN) o.w[r - TM] = *reinterpret_cast<const uint4_t*>(stg + w_rd + (r - TM) * 1024);
+    else if (r == TM + TN) o.sa = *reinterpret_cast<const uint32_t*>(stg + as_rd);
+    else o.sw = *reinterpret_cast<const uint32_t*>(stg + ws_rd) >> ws_shift;
+  };
+  constexpr int kReads = TM + TN + 2;
+  auto mfma_one = [&](const Ops& o, int q) {
+    const int i = q / TN, j = q % TN;
+    const int8v_t av = {(int)o.a[i][0], (int)o.a[i][1], (int)o.a[i][2], (int)o.a[i][3], 0, 0, 0, 0};
+    const int8v_t wv = {(int)o.w[j][0], (int)o.w[j][1], (int)o.w[j][2], (int)o.w[j][3], 0, 0, 0, 0};
+    // W as the first operand: the accumulator block is the transposed output
+    // tile, so each lane ends up with 4 consecutive output columns.  E2M1 is
+    // format 4 for both operands; op_sel picks the tile's scale byte.
+    switch (i * 4 + j) {
+#define DQ_MX_MFMA(I, J)                                                                                     \
+  case I * 4 + J:                                                                                            \
+    if constexpr (J < TN)                                                                                    \
+      acc[I][J] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wv, av, acc[I][J], 4, 4, J, (int)o.sw, I,    \
+                                                                 (int)o.sa);                                 \
+    break;
+      DQ_MX_MFMA(0, 0) DQ_MX_MFMA(0, 1) DQ_MX_MFMA(0, 2) DQ_MX_MFMA(0, 3)
+      DQ_MX_MFMA(1, 0) DQ_MX_MFMA(1, 1) DQ_MX_MFMA(1, 2) DQ_MX_MFMA(1, 3)
+      DQ_MX_MFMA(2, 0) DQ_MX_MFMA(2, 1) DQ_MX_MFMA(2, 2) DQ_MX_MFMA(2, 3)
+      DQ_MX_MFMA(3, 0) DQ_MX_MFMA(3, 1) DQ_MX_MFMA(3, 2) DQ_MX_MFMA(3, 3)
+#undef DQ_MX_MFMA
+      default: break;
     }
   };
-  auto mfmas = [&](const Ops& o) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int8v_t av = {(int)o.a[i][0], (int)o.a[i][1], (int)o.a[i][2], (int)o.a[i][3], 0, 0, 0, 0};
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int8v_t wv = {(int)o.w[j][0], (int)o.w[j][1], (int)o.w[j][2], (int)o.w[j][3], 0, 0, 0, 0};
-        // A and W in E2M1 (format 4), scales in byte 0 of the scale operands
-        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, wv, acc[i][j], 4, 4, 0, (int)o.sa[i], 0,
-                                                                   (int)o.sw[j]);
-      }
-    }
-  };
-  // this wavefront's loads of stage `need` have landed, with stages up to
-  // `last` issued
-  auto wait_stage = [&](int need, int last) {
-    const int ahead = max(0, min(last, KTi - 1) - need);
-    static_assert(S - 2 <= 4 && 4 * L <= 63, "wait table");
-    if (ahead >= 4) mx_wait_vm<4 * L>();
-    else if (ahead == 3) mx_wait_vm<3 * L>();
-    else if (ahead == 2) mx_wait_vm<2 * L>();
-    else if (ahead == 1) mx_wait_vm<L>();
-    else mx_wait_vm<0>();
-  };
+  constexpr int kMfmas = TM * TN;
+  constexpr int kSlots = kMfmas > kReads + 3 ? kMfmas : kReads + 3;
 
-  // prologue: stages 0 .. S-1 in flight, stage 0 landed everywhere
+  if (KTi > 0) {
+    // prologue: stages 0 .. S-1 in flight, stage 0 landed everywhere
 #pragma unroll
-  for (int s = 0; s < S; ++s)
-    if (s < KTi) issue(s);
-  wait_stage(0, S - 1);
-  mx_barrier();
-  Ops o0, o1;
-  read_ops(0, o0);
-  // Step kt (operands of stage kt in `cur`, read during the previous step):
-  // wait for this wavefront's loads of stage kt+1 and for this wavefront's
-  // reads of stage kt, then the barrier: stage kt+1 has landed everywhere and
-  // every wavefront is done with stage kt's slot, which is refilled with
-  // stage kt+S.  Stage kt+1's operands are read while step kt's MFMAs run.
-  // The sched_barriers keep the compiler from sinking the MFMAs past the
-  // next step's waits and barrier (the matrix cores would idle through them).
-  auto step = [&](int kt, Ops& cur, Ops& nxt) {
-    const bool more = kt + 1 < KTi;
-    if (more) wait_stage(kt + 1, kt + S - 1);
-    __builtin_amdgcn_s_waitcnt((0x3F & 0xF) | (0x7 << 4) | (0x0 << 8) | ((0x3F >> 4) << 14));   // lgkmcnt(0)
+    for (int st = 0; st < S; ++st) issue(st);
+    mx_wait_vm<(S - 1) * L>();
     mx_barrier();
-    if (kt + S < KTi) issue(kt + S);
-    if (more) read_ops(kt + 1, nxt);
-    __builtin_amdgcn_sched_barrier(0);
-    mfmas(cur);
-    __builtin_amdgcn_sched_barrier(0);
-  };
-  int kt = 0;
-  for (; kt + 1 < KTi; kt += 2) {
-    step(kt, o0, o1);
-    step(kt + 1, o1, o0);
+    Ops o0, o1;
+    // One step (cur = stage kt's operands, read during the previous step):
+    // two MFMAs are issued before the wait for stage kt+1 and the barrier so
+    // that the matrix cores stay busy through them; after the barrier the
+    // slot of stage kt (read by everyone) is refilled with stage kt+S and the
+    // reads of stage kt+1 are interleaved with the remaining MFMAs.  The
+    // sched_barriers keep this order; the empty asm statements pin the
+    // accumulators at the end of the step (otherwise the compiler sinks the
+    // MFMAs, pure register operations, into the next step).
+    auto step = [&](int kt, Ops& cur, Ops& nxt) {
+      __builtin_amdgcn_s_waitcnt((0x3F & 0xF) | (0x7 << 4) | (0x0 << 8) | ((0x3F >> 4) << 14));   // lgkmcnt(0)
+      mfma_one(cur, 0);
+      mfma_one(cur, 1);
+      __builtin_amdgcn_sched_barrier(0);
+      mx_wait_vm<(S - 2) * L>();
+      mx_barrier();
+      mfma_one(cur, 2);
+      __builtin_amdgcn_sched_barrier(0);
+      issue(kt + S);
+      const uint8_t* stg = smem + ((kt + 1) % S) * Gm::bytes;
+#pragma unroll
+      for (int q = 3; q < kSlots; ++q) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (q - 3 < kReads) read_one(stg, nxt, q - 3);
+        __builtin_amdgcn_sched_barrier(0);
+        if (q < kMfmas) mfma_one(cur, q);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) asm volatile("" : "+a"(acc[i][j]));
+    };
+    // Full steps 0 .. KT-2 alternate o0 -> o1 and o1 -> o0; the first one is
+    // peeled when their number is odd, so that the last step always consumes o0.
+    const int full = KTi - 1;
+    int kt = 0;
+    if (full & 1) {
+#pragma unroll
+      for (int r = 0; r < kReads; ++r) read_one(smem, o1, r);
+      step(0, o1, o0);
+      kt = 1;
+    } else {
+#pragma unroll
+      for (int r = 0; r < kReads; ++r) read_one(smem, o0, r);
+    }
+    for (; kt < full; kt += 2) {
+      step(kt, o0, o1);
+      step(kt + 1, o1, o0);
+    }
+    __builtin_amdgcn_s_waitcnt((0x3F & 0xF) | (0x7 << 4) | (0x0 << 8) | ((0x3F >> 4) << 14));   // lgkmcnt(0)
+#pragma unroll
+    for (int q = 0; q < kMfmas; ++q) mfma_one(o0, q);
+    // drain the redundant reloads of the last steps before the workgroup ends
+    mx_wait_vm<0>();
   }
-  if (kt < KTi) step(kt, o0, o1);
 
-  const int col_in = lane & 31;
-  const int row_off = 4 * (lane >> 5);
+  // Block (i, j) holds, in lane l, output row m0 + 32i + l%32 and columns
+  // n0 + 32j + 8g + 4(l/32) + t in register 4g + t (g, t = 0..3): four
+  // consecutive columns, stored as one 8-byte (bf16) or 16-byte (fp32) write
+  // when the row stride keeps them aligned (N % 4 == 0).
+  const bool vec = (N & 3) == 0;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
+    const int64_t row = m0 + i * 32 + (lane & 31);
+    if (row >= M) continue;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      const int64_t col = n0 + j * 32 + col_in;
-      if (col >= N) continue;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + i * 32 + 8 * (r >> 2) + row_off + (r & 3);
-        if (row < M) {
-          if (OUT == 0)
-            reinterpret_cast<float*>(Y)[row * N + col] = acc[i][j][r];
-          else
-            reinterpret_cast<uint16_t*>(Y)[row * N + col] = (uint16_t)f32_to_bf16_rne(acc[i][j][r]);
+      for (int g = 0; g < 4; ++g) {
+        const int64_t col = n0 + j * 32 + g * 8 + 4 * (lane >> 5);
+        const float v0 = acc[i][j][4 * g], v1 = acc[i][j][4 * g + 1], v2 = acc[i][j][4 * g + 2],
+                    v3 = acc[i][j][4 * g + 3];
+        if (OUT == 0) {
+          float* y = reinterpret_cast<float*>(Y) + row * N + col;
+          if (vec && col + 3 < N) {
+            *reinterpret_cast<float4_t*>(y) = float4_t{v0, v1, v2, v3};
+          } else {
+            if (col < N) y[0] = v0;
+            if (col + 1 < N) y[1] = v1;
+            if (col + 2 < N) y[2] = v2;
+            if (col + 3 < N) y[3] = v3;
+          }
+        } else {
+          const uint32_t b0 = f32_to_bf16_rne(v0), b1 = f32_to_bf16_rne(v1), b2 = f32_to_bf16_rne(v2),
+                         b3 = f32_to_bf16_rne(v3);
+          uint16_t* y = reinterpret_cast<uint16_t*>(Y) + row * N + col;
+          if (vec && col + 3 < N) {
+            *reinterpret_cast<uint2_t*>(y) = uint2_t{b0 | (b1 << 16), b2 | (b3 << 16)};
+          } else {
+            if (col < N) y[0] = (uint16_t)b0;
+            if (col + 1 < N) y[1] = (uint16_t)b1;
+            if (col + 2 < N) y[2] = (uint16_t)b2;
+            if (col + 3 < N) y[3] = (uint16_t)b3;
+          }
         }
       }
     }
@@ -353,9 +436,9 @@ hipError_t launch_mx_geo(const MxGemmArgs& a, int64_t n_off, int64_t n_end, hipS
 hipError_t launch_mx_quantize(const void* x, bool is_bf16, int64_t rows, int64_t cols, const MxView& out,
                               hipStream_t s) {
   const int64_t tiles_r = round_up(rows, 32) / 32, tiles_c = round_up(cols, 64) / 64;
-  const int64_t tiles = tiles_r * tiles_c;
-  if (tiles == 0) return hipSuccess;
-  const unsigned grid = (unsigned)((tiles + 3) / 4);
+  const int64_t groups = (tiles_r + 3) / 4 * tiles_c;
+  if (groups == 0) return hipSuccess;
+  const unsigned grid = (unsigned)groups;
   if (is_bf16)
     hipLaunchKernelGGL(mx_quantize_kernel<uint16_t>, dim3(grid), dim3(256), 0, s, static_cast<const uint16_t*>(x),
                        rows, cols, tiles_r, tiles_c, out.codes, out.scales);
@@ -367,9 +450,17 @@ hipError_t launch_mx_quantize(const void* x, bool is_bf16, int64_t rows, int64_t
 
 hipError_t launch_mx_gemm(const MxGemmArgs& a, hipStream_t s) {
   if (a.M == 0 || a.N == 0) return hipSuccess;
-  // 256x256 workgroup tiles: four wavefronts of 128x128, one per SIMD
+  // 256x256 workgroup tiles (four wavefronts of 128x128, one per SIMD); one
+  // workgroup fills a compute unit, so a last round that would leave compute
+  // units idle runs instead as a second launch of 256x128 tiles over the
+  // remaining column panels.
   using Full = MxGeo<4, 4, 2, 2>;
-  return launch_mx_geo<Full>(a, 0, a.N, s);
+  using Half = MxGeo<4, 2, 2, 2>;
+  const int64_t n_split = gemm_column_split(a.M, a.N, Full::bm, Full::bn, Half::bn, num_cus());
+  hipError_t e = hipSuccess;
+  if (n_split > 0) e = launch_mx_geo<Full>(a, 0, n_split, s);
+  if (e == hipSuccess && n_split < a.N) e = launch_mx_geo<Half>(a, n_split, a.N, s);
+  return e;
 }
 
 }  // namespace dq

@@ -54,8 +54,10 @@ def mxfp4_unpack(codes: np.ndarray, scales: np.ndarray, rows: int, cols: int):
     q[..., 0::2] = cb & 0xF
     q[..., 1::2] = cb >> 4
     q = q.transpose(0, 2, 1, 3).reshape(R, C)
-    # tile scale byte r + 32h = row r, 32-block h of the tile
-    sb = np.asarray(scales, np.uint8)[: R * C // 32].reshape(tr, tc, 2, 32).transpose(0, 3, 1, 2).reshape(R, C // 32)
+    # 4-tile scale groups: byte 4*(r + 32h) + q of group (g, tc) = row 128g + 32q + r, block 2tc + h
+    R4 = _ru(rows, 128)
+    sb = (np.asarray(scales, np.uint8)[: R4 * C // 32].reshape(R4 // 128, tc, 2, 32, 4)
+          .transpose(0, 4, 3, 1, 2).reshape(R4, C // 32))
     return q[:rows, :cols], sb[:rows, : cols // 32], q, sb
 
 
@@ -65,12 +67,14 @@ def mxfp4_pack(codes: np.ndarray, scale_codes: np.ndarray):
     R, C = _ru(rows, 32), _ru(cols, 64)
     q = np.zeros((R, C), np.uint8)
     q[:rows, :cols] = codes
-    s = np.zeros((R, C // 32), np.uint8)
+    R4 = _ru(rows, 128)
+    s = np.zeros((R4, C // 32), np.uint8)
     s[:rows, : cols // 32] = scale_codes
     tr, tc = R // 32, C // 64
     qt = q.reshape(tr, 32, tc, 64).transpose(0, 2, 1, 3)
     cb = (qt[..., 0::2] | (qt[..., 1::2] << 4)).astype(np.uint8).reshape(-1)
-    sb = s.reshape(tr, 32, tc, 2).transpose(0, 2, 3, 1).reshape(-1).astype(np.uint8)
+    # [g, q, r, tc, h] -> [g, tc, h, r, q]
+    sb = s.reshape(R4 // 128, 4, 32, tc, 2).transpose(0, 3, 4, 2, 1).reshape(-1).astype(np.uint8)
     return cb, sb
 
 

@@ -49,6 +49,7 @@ def test_size_queries():
     with pytest.raises(dq.DQError):
         dq.lut_sizes(3, 0, 16, 48)
     assert dq.mxfp4_sizes(100, 96) == (128 * 128 // 2, 128 * 128 // 32)
+    assert dq.mxfp4_sizes(130, 64) == (160 * 64 // 2, 256 * 64 // 32)
     assert dq.mxfp4_sizes(0, 0) == (0, 0)
     with pytest.raises(dq.DQError):
         dq.mxfp4_sizes(4, 48)
