@@ -145,6 +145,47 @@ def cpu_baseline(cfg, w, X, G_x, xds, min_seconds=10.0):
     }
 
 
+def mxfp4_prefill(dq, torch, np, w, Xs, M, N, K, s, reps):
+    """The MXFP4 W4A4 variant of the same prefill linear (OCP MX: E8M0 scale
+    per 32, block scales applied inside the FP4 MFMA), timed apart from the
+    NVFP4 steps: activation quantization and GEMM with HIP events around
+    `reps` calls of each."""
+    lib = dq.lib()
+    sp = ctypes.c_void_p(s.cuda_stream)
+    Wm = dq.dq_pack_mxfp4(torch.from_numpy(np.ascontiguousarray(w)).cuda())
+    A = dq.MxFp4Tensor.empty(M, K)
+    Y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    dA, dW = A.desc(), Wm.desc()
+    n_x = len(Xs)
+
+    def quant(i):
+        return lib.dq_quantize_act_mxfp4(ctypes.c_void_p(Xs[i % n_x].data_ptr()), M, K, ctypes.byref(dA), sp)
+
+    def gemm():
+        return lib.dq_prefill_gemm_mxfp4(ctypes.byref(dA), ctypes.byref(dW), dq.OUT_BF16,
+                                         ctypes.c_void_p(Y.data_ptr()), sp)
+    for i in range(3):
+        assert quant(i) == 0 and gemm() == 0
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    ev[0].record(s)
+    for i in range(reps):
+        assert quant(i) == 0
+    ev[1].record(s)
+    for _ in range(reps):
+        assert gemm() == 0
+    ev[2].record(s)
+    torch.cuda.synchronize()
+    t_q = ev[0].elapsed_time(ev[1]) / reps * 1e-3
+    t_g = ev[1].elapsed_time(ev[2]) / reps * 1e-3
+    flops = 2.0 * M * N * K
+    return {"quant_us": t_q * 1e6, "quant_GB/s": M * K * (2 + 0.5 + 1 / 32) / t_q / 1e9,
+            "gemm_us": t_g * 1e6, "gemm_TFLOP/s": flops / t_g / 1e12,
+            "frac_fp4_peak": flops / t_g / 1e12 / PEAK_FP4_TFLOPS,
+            "linear_TFLOP/s_incl_quant": flops / (t_q + t_g) / 1e12,
+            "note": "MXFP4 W4A4 (E2M1, E8M0 per 32 along K) on the scaled FP4 MFMA; same shapes and bf16 output"}
+
+
 def decode_sweep(dq, synth, torch, np, n_blocks, steps):
     """One decode token through n_blocks stacked 27B-class blocks (distinct
     copies of one packed block), LUT3 at batch 1, 8, 16 and LUT2 at batch 1."""
@@ -348,6 +389,7 @@ def main():
                      "note": "exact NVFP4 operands are dequantized to fp16 and multiplied on fp16 MFMA; "
                              "frac of the dense FP4 peak is prefill.frac_fp4_peak"},
     }
+    out["mxfp4_prefill"] = mxfp4_prefill(dq, torch, np, w, Xs, M, N, K, s, args.steps)
     del Wls, dWls, Xs
     torch.cuda.empty_cache()
     if not args.no_decode_sweep:
