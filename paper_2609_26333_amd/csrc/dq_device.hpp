@@ -87,6 +87,31 @@ __device__ inline void atomic_max_nonneg(float* p, float v) {
   atomicMax(reinterpret_cast<unsigned int*>(p), __float_as_uint(v));
 }
 
+// ---------------------------------------------------------------- GEMM tile order
+// Output tile of workgroup b.  Tiles are ordered in bands of GM row panels,
+// row panel fastest within a band, so that the ~256 workgroups in flight at
+// once cover about GM x 256/GM tiles and share their A and W panels through
+// the L2 and the MALL.  Workgroup b runs on XCD b % 8; within each complete
+// group of 256 workgroups the 32 of one XCD take a 4 x 8 sub-block, so each
+// XCD's L2 streams 12 panels instead of up to 33.
+__device__ inline void gemm_tile_of(int64_t b, int64_t tiles_m, int64_t tiles_n, int64_t& bm, int64_t& bn) {
+  const int64_t nb = tiles_m * tiles_n;
+  const int GM = tiles_m >= 16 ? 16 : tiles_m >= 8 ? 8 : tiles_m >= 4 ? 4 : (int)tiles_m;
+  int64_t L = b;
+  if ((GM == 4 || GM == 8 || GM == 16) && (b | 255) < nb) {
+    const int q = (int)(b & 255), xcd = q & 7, loc = q >> 3;
+    const int xm = GM / 4;
+    const int m_in = (xcd % xm) * 4 + (loc & 3), n_in = (xcd / xm) * 8 + (loc >> 2);
+    L = b - q + m_in + GM * n_in;
+  }
+  const int64_t band = L / (GM * tiles_n);
+  const int64_t first = band * GM;
+  const int64_t gm = tiles_m - first < GM ? tiles_m - first : GM;
+  const int64_t idx = L - band * GM * tiles_n;
+  bm = first + idx % gm;
+  bn = idx / gm;
+}
+
 // ---------------------------------------------------------------- wave ops
 __device__ inline float wave_max(float v) {
 #pragma unroll

@@ -32,7 +32,7 @@
 //  * the operands of K step kt+1 are read from LDS into registers while the
 //    MFMAs of step kt run;
 //  * output tiles are handed out in bands of row panels, with each XCD taking
-//    a compact sub-block of the tiles in flight (see tile_of).
+//    a compact sub-block of the tiles in flight (see gemm_tile_of).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -173,30 +173,6 @@ __device__ inline void mx_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Output tile of workgroup b.  Tiles are ordered in bands of GM row panels,
-// row panel fastest within a band, so that the ~256 workgroups in flight at
-// once cover about GM x 256/GM tiles and share their A and W panels through
-// the L2 and the MALL.  Workgroup b runs on XCD b % 8; within each complete
-// group of 256 workgroups the 32 of one XCD take a 4 x 8 sub-block, so each
-// XCD's L2 streams 12 panels instead of up to 33.
-__device__ inline void tile_of(int64_t b, int64_t tiles_m, int64_t tiles_n, int64_t& bm, int64_t& bn) {
-  const int64_t nb = tiles_m * tiles_n;
-  const int GM = tiles_m >= 16 ? 16 : tiles_m >= 8 ? 8 : tiles_m >= 4 ? 4 : (int)tiles_m;
-  int64_t L = b;
-  if ((GM == 4 || GM == 8 || GM == 16) && (b | 255) < nb) {
-    const int q = (int)(b & 255), xcd = q & 7, loc = q >> 3;
-    const int xm = GM / 4;
-    const int m_in = (xcd % xm) * 4 + (loc & 3), n_in = (xcd / xm) * 8 + (loc >> 2);
-    L = b - q + m_in + GM * n_in;
-  }
-  const int64_t band = L / (GM * tiles_n);
-  const int64_t first = band * GM;
-  const int64_t gm = tiles_m - first < GM ? tiles_m - first : GM;
-  const int64_t idx = L - band * GM * tiles_n;
-  bm = first + idx % gm;
-  bn = idx / gm;
-}
-
 template <class Gm, int OUT>
 __global__ __launch_bounds__(Gm::threads, 1) void mxfp4_gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales, const uint8_t* __restrict__ w_codes,
@@ -210,7 +186,7 @@ __global__ __launch_bounds__(Gm::threads, 1) void mxfp4_gemm_kernel(
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   int64_t bm, bn;
-  tile_of(blockIdx.x, tiles_m, tiles_n, bm, bn);
+  gemm_tile_of(blockIdx.x, tiles_m, tiles_n, bm, bn);
   const int wm = wave % Gm::wm, wn = wave / Gm::wm;
   const int64_t a_tr0 = bm * Gm::at, w_tr0 = n_off / 32 + bn * Gm::wt;
   const int64_t m0 = bm * Gm::bm + wm * 32 * TM;
