@@ -21,9 +21,12 @@ one decode token through 64 stacked 27B-class blocks (q/k/v 7168x5120,
 o 5120x5120, gate/up 34816x5120, down 5120x17408: 7.93 GB of LUT3 codes, all
 distinct memory) at batch 1, 8 and 16, and the same in LUT2 at batch 1.
 
-Prints one JSON line.  `value` is the prefill linear throughput: 2*M*N*K over
-(quantization + GEMM) time.  Per-kernel durations come from HIP events
-recorded on the launch stream around every kernel of the timed steps.
+Prints one JSON line.  `ms_per_step` is the time of the timed steps (HIP
+events on the launch stream around them, nothing else in between).  `value`
+is the prefill linear throughput: 2*M*N*K over (quantization + GEMM) time,
+each measured as back-to-back calls of that kernel alone between one pair of
+events (the average includes the GPU-side gap between launches, no host or
+event overhead); the GEMV rates are measured the same way.
 
 `--calibrate-copy` instead runs a plain 256 MiB device copy five times: the
 reference kernel whose FETCH_SIZE / WRITE_SIZE readings scale the GEMM's
@@ -317,37 +320,45 @@ def main():
         return lib.dq_decode_gemv(ctypes.c_void_p(xd_dev[b].data_ptr()), b, ctypes.byref(dWls[i % n_w]),
                                   dq.OUT_F32, ctypes.c_void_p(ys[b].data_ptr()), wsp, ws_n, sp)
 
-    names = ["quant", "gemm"] + [f"gemv_b{b}" for b in Bs]
-
-    def step(i, evs):
-        if evs:
-            evs[0].record(s)
+    def step(i):
         assert quant(i) == 0
-        if evs:
-            evs[1].record(s)
         assert gemm() == 0
-        if evs:
-            evs[2].record(s)
         for j, b in enumerate(Bs):
             assert gemv(i * len(Bs) + j, b) == 0
-            if evs:
-                evs[3 + j].record(s)
 
     for i in range(args.warmup):
-        step(i, None)
+        step(i)
     torch.cuda.synchronize()
-    n_ev = 3 + len(Bs)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(args.steps)]
+    # the timed steps: nothing but the step's launches between the two events
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     t_start.record(s)
     for i in range(args.steps):
-        step(args.warmup + i, evs[i])
+        step(args.warmup + i)
     t_end.record(s)
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
-    per = {n: float(np.mean([evs[i][k].elapsed_time(evs[i][k + 1]) for i in range(args.steps)]))
-           for k, n in enumerate(names)}
+
+    # per-kernel rates: `reps` back-to-back calls of one kernel (rotating the
+    # activation copies and decode weight copies) between one pair of events,
+    # so the average includes the GPU-side gap between launches but no event
+    # or host overhead
+    reps = max(20, args.steps)
+
+    def back_to_back(fn):
+        for i in range(3):
+            fn(i)
+        torch.cuda.synchronize()
+        ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ea.record(s)
+        for i in range(reps):
+            fn(i)
+        eb.record(s)
+        torch.cuda.synchronize()
+        return ea.elapsed_time(eb) / reps
+
+    per = {"quant": back_to_back(lambda i: quant(i)), "gemm": back_to_back(lambda i: gemm())}
+    for b in Bs:
+        per[f"gemv_b{b}"] = back_to_back(lambda i, b=b: gemv(i, b))
 
     flops = 2.0 * M * N * K
     quant_bytes = M * K * 2 + M * K / 2 + M * K / 16
