@@ -189,6 +189,43 @@ def mxfp4_prefill(dq, torch, np, w, Xs, M, N, K, s, reps):
             "note": "MXFP4 W4A4 (E2M1, E8M0 per 32 along K) on the scaled FP4 MFMA; same shapes and bf16 output"}
 
 
+def nvfp4a16_decode(dq, torch, np, Wq, xd_dev, Bs, N, K, s, decode_bytes, reps):
+    """Weight-only NVFP4 decode GEMV (format-disaggregated NVFP4) over the same
+    packed NVFP4 weights the prefill GEMM uses, at the decode batches, with
+    the weights rotated over enough copies to stream from HBM."""
+    lib = dq.lib()
+    sp = ctypes.c_void_p(s.cuda_stream)
+    nbytes = Wq.codes.numel() + Wq.scales.numel()
+    n_w = max(2, -(-decode_bytes // nbytes))
+    Ws = [Wq] + [dq.NvFp4Tensor(Wq.codes.clone(), Wq.scales.clone(), Wq.G.clone(), N, K) for _ in range(n_w - 1)]
+    ds = [x.desc() for x in Ws]
+    out = {}
+    for b in Bs:
+        y = torch.empty((b, N), dtype=torch.float32, device="cuda")
+        ws_n = dq.dq_decode_gemv_nvfp4_workspace_size(b, Wq)
+        ws = torch.empty(max(ws_n, 16), dtype=torch.uint8, device="cuda")
+        args_ = (ctypes.c_void_p(xd_dev[b].data_ptr()), b)
+        call = lambda i: lib.dq_decode_gemv_nvfp4(*args_, ctypes.byref(ds[i % n_w]), dq.OUT_F32,  # noqa: E731
+                                                 ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
+                                                 ws_n, sp)
+        for i in range(n_w):
+            assert call(i) == 0
+        torch.cuda.synchronize()
+        ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ea.record(s)
+        for i in range(reps):
+            call(i)
+        eb.record(s)
+        torch.cuda.synchronize()
+        t = ea.elapsed_time(eb) / reps * 1e-3
+        alg = nbytes + b * K * 2 + b * N * 4
+        out[f"b{b}"] = {"us": t * 1e6, "GB/s": alg / t / 1e9, "frac_hbm": alg / t / 1e9 / PEAK_HBM_GBS,
+                        "bytes": alg}
+    out["weight_copies"] = n_w
+    out["note"] = "NVFP4 weights (4.5 bits), bf16 x, fp16 MFMA; back-to-back calls incl. the K-group reduction pass"
+    return out
+
+
 def decode_sweep(dq, synth, torch, np, n_blocks, steps):
     """One decode token through n_blocks stacked 27B-class blocks (distinct
     copies of one packed block), LUT3 at batch 1, 8, 16 and LUT2 at batch 1."""
@@ -401,6 +438,7 @@ def main():
                              "frac of the dense FP4 peak is prefill.frac_fp4_peak"},
     }
     out["mxfp4_prefill"] = mxfp4_prefill(dq, torch, np, w, Xs, M, N, K, s, args.steps)
+    out["nvfp4a16_decode"] = nvfp4a16_decode(dq, torch, np, Wq, xd_dev, Bs, N, K, s, args.decode_bytes, reps)
     del Wls, dWls, Xs
     torch.cuda.empty_cache()
     if not args.no_decode_sweep:

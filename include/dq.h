@@ -228,6 +228,21 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
                           const float* G_out_static, const dq_nvfp4_t* Yq, int epilogue_flags,
                           void* stream);
 
+/* ---- NVFP4A16 decode GEMV ------------------------------------------------
+ * The weight-only NVFP4 decode of format disaggregation (Sec. 3: decode
+ * keeps 16-bit activations and quantizes only the weights; App. A "NVFP4"):
+ * y[b, n] = sum_k x[b, k] * w_hat[n, k], w_hat = e2m1 * e4m3(scale) * G.
+ * x: device bf16 [B, K] row-major, 1 <= B <= 16.  W: NVFP4 weights as packed
+ * by dq_pack_nvfp4 (rows = N, cols = K).  out_kind DQ_OUT_F32 / DQ_OUT_BF16:
+ * y is device [B, N] row-major.  workspace / workspace_bytes as for
+ * dq_decode_gemv (partial sums over K groups; NULL takes stream-ordered
+ * memory from the library's pool).  Activations are staged as fp16 after a
+ * power-of-two rescale per batch row and K group (the conversion described
+ * for dq_decode_gemv); weight products are exact, sums fp32. */
+dq_status dq_decode_gemv_nvfp4_workspace_size(int64_t B, const dq_nvfp4_t* W, size_t* bytes);
+dq_status dq_decode_gemv_nvfp4(const uint16_t* x, int64_t B, const dq_nvfp4_t* W, int out_kind, void* y,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
 /* ---- MXFP4 W4A4 prefill variant ------------------------------------------
  * Quantization of a 32-block with largest magnitude a (OCP MX conversion):
  * e = floor(log2 a) - 2, clamped to [-127, 127] (-127 for an all-zero block),

@@ -47,6 +47,13 @@ def lut_gemv_paper(x_bits, codes, scale_bytes, G, grid) -> np.ndarray:
     return gemv_bf16(x_bits, lut.dequantize_paper_grid(codes, scale_bytes, G, grid))
 
 
+def nvfp4a16_gemv(x_bits, codes, scale_codes, G) -> np.ndarray:
+    """Weight-only NVFP4 decode (Sec. 3, format disaggregation: 16-bit
+    activations, NVFP4 weights): ``y[b, n] = sum_k x[b, k] * w_hat[n, k]`` with
+    the NVFP4 dequantization of App. A, in fp64."""
+    return gemv_bf16(x_bits, nvfp4.dequantize(codes, scale_codes, G))
+
+
 def silu_mul(g, u) -> np.ndarray:
     """SwiGLU's ``silu(g) * u = g / (1 + exp(-g)) * u`` in fp64."""
     g = np.asarray(g, np.float64)

@@ -67,6 +67,8 @@ def _load() -> ctypes.CDLL:
         "dq_quantize_act_nvfp4": (S, [P, I64, I64, P, ctypes.POINTER(_NvFp4), P]),
         "dq_prefill_gemm": (S, [ctypes.POINTER(_NvFp4), P, P, ctypes.POINTER(_NvFp4), I64, I32, P, P,
                                 ctypes.POINTER(_NvFp4), I32, P]),
+        "dq_decode_gemv_nvfp4_workspace_size": (S, [I64, ctypes.POINTER(_NvFp4), SZ]),
+        "dq_decode_gemv_nvfp4": (S, [P, I64, ctypes.POINTER(_NvFp4), I32, P, P, ctypes.c_size_t, P]),
         "dq_mxfp4_sizes": (S, [I64, I64, SZ, SZ]),
         "dq_pack_mxfp4": (S, [P, I64, I64, ctypes.POINTER(_MxFp4), P]),
         "dq_quantize_act_mxfp4": (S, [P, I64, I64, ctypes.POINTER(_MxFp4), P]),
@@ -85,7 +87,8 @@ _lib = _load()
 EXPORTED = ("dq_abi_version", "dq_status_string", "dq_last_error", "dq_nvfp4_sizes", "dq_lut_sizes",
             "dq_pack_nvfp4", "dq_pack_lut3", "dq_quantize_act_nvfp4", "dq_prefill_gemm",
             "dq_decode_gemv_workspace_size", "dq_decode_gemv", "dq_mxfp4_sizes", "dq_pack_mxfp4",
-            "dq_quantize_act_mxfp4", "dq_prefill_gemm_mxfp4")
+            "dq_quantize_act_mxfp4", "dq_prefill_gemm_mxfp4", "dq_decode_gemv_nvfp4_workspace_size",
+            "dq_decode_gemv_nvfp4")
 
 
 def lib() -> ctypes.CDLL:
@@ -303,6 +306,38 @@ def dq_prefill_gemm_mxfp4(A: MxFp4Tensor, W: MxFp4Tensor, out_kind: int = OUT_F3
 
 
 _gemv_ws_cache: dict = {}
+
+
+def dq_decode_gemv_nvfp4_workspace_size(B: int, W: NvFp4Tensor) -> int:
+    """Workspace bytes dq_decode_gemv_nvfp4 needs for batch B."""
+    key = ("nvfp4", B, W.rows, W.cols, W.codes.device.index)
+    n = _gemv_ws_cache.get(key)
+    if n is None:
+        out = ctypes.c_size_t()
+        _check(_lib.dq_decode_gemv_nvfp4_workspace_size(B, ctypes.byref(W.desc()), ctypes.byref(out)),
+               "dq_decode_gemv_nvfp4_workspace_size")
+        n = _gemv_ws_cache[key] = out.value
+    return n
+
+
+def dq_decode_gemv_nvfp4(x: torch.Tensor, W: NvFp4Tensor, out_kind: int = OUT_F32, y: Optional[torch.Tensor] = None,
+                         stream=None, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    x = _as_u16(x)
+    assert x.is_contiguous() and x.dim() == 2
+    B = x.shape[0]
+    if y is None:
+        y = torch.empty((B, W.rows), dtype=torch.float32 if out_kind == OUT_F32 else torch.bfloat16,
+                        device=x.device)
+    if workspace is None:
+        n = dq_decode_gemv_nvfp4_workspace_size(B, W)
+        if n:
+            workspace = torch.empty(n, dtype=torch.uint8, device=x.device)
+    ws_ptr, ws_bytes = (workspace.data_ptr(), workspace.numel() * workspace.element_size()) if workspace is not None \
+        else (None, 0)
+    d = W.desc()
+    _check(_lib.dq_decode_gemv_nvfp4(x.data_ptr(), B, ctypes.byref(d), out_kind, y.data_ptr(), ws_ptr, ws_bytes,
+                                     _stream(stream)), "dq_decode_gemv_nvfp4")
+    return y
 
 
 def dq_decode_gemv_workspace_size(B: int, W: LutWeight) -> int:

@@ -22,7 +22,7 @@ ARCH = "gfx950"
 # Quantizers (and the GEMM's requantizing epilogue) must round exactly as
 # written: no contraction of a*b+c.
 EXACT_TUS = {"quant.hip", "pack_lut.hip", "gemm.hip", "mxfp4.hip"}
-SOURCES = ["quant.hip", "pack_lut.hip", "gemm.hip", "gemv.hip", "mxfp4.hip", "dq_api.cpp"]
+SOURCES = ["quant.hip", "pack_lut.hip", "gemm.hip", "gemv.hip", "gemv_nvfp4.hip", "mxfp4.hip", "dq_api.cpp"]
 
 
 def hipcc() -> str:

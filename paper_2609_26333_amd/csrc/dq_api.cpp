@@ -331,6 +331,38 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
   return hip_status(e, "dq_prefill_gemm");
 }
 
+dq_status dq_decode_gemv_nvfp4_workspace_size(int64_t B, const dq_nvfp4_t* W, size_t* bytes) {
+  if (W == nullptr) return fail(DQ_ERR_INVALID_ARG, "W is NULL");
+  if (W->rows < 0 || W->cols < 0 || W->cols % 16 != 0)
+    return fail(DQ_ERR_INVALID_ARG, "W: rows >= 0, cols >= 0 and cols %% 16 == 0 required");
+  if (B < 1 || B > 16) return fail(DQ_ERR_INVALID_ARG, "1 <= B <= 16 required");
+  if (bytes == nullptr) return fail(DQ_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = dq::gemv_nvfp4_workspace_bytes(B, W->rows, W->cols);
+  return DQ_OK;
+}
+
+dq_status dq_decode_gemv_nvfp4(const uint16_t* x, int64_t B, const dq_nvfp4_t* W, int out_kind, void* y,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  if (W == nullptr) return fail(DQ_ERR_INVALID_ARG, "W is NULL");
+  dq_status st = check_nvfp4(W, "W", W->rows, W->cols);
+  if (st != DQ_OK) return st;
+  if (W->rows < 0 || W->cols < 0 || W->cols % 16 != 0)
+    return fail(DQ_ERR_INVALID_ARG, "W: rows >= 0, cols >= 0 and cols %% 16 == 0 required");
+  if (B < 1 || B > 16) return fail(DQ_ERR_INVALID_ARG, "1 <= B <= 16 required");
+  if ((x == nullptr && W->cols > 0) || !aligned(x, 16))
+    return fail(DQ_ERR_INVALID_ARG, "x must be 16-byte aligned and non-NULL unless K == 0");
+  if (out_kind != DQ_OUT_F32 && out_kind != DQ_OUT_BF16) return fail(DQ_ERR_INVALID_ARG, "bad out_kind");
+  if (y == nullptr && W->rows > 0) return fail(DQ_ERR_INVALID_ARG, "y is NULL");
+  if (!aligned(y, 16)) return fail(DQ_ERR_INVALID_ARG, "y must be 16-byte aligned");
+  if (workspace != nullptr) {
+    if (!aligned(workspace, 16)) return fail(DQ_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+    if (workspace_bytes < dq::gemv_nvfp4_workspace_bytes(B, W->rows, W->cols))
+      return fail(DQ_ERR_INVALID_ARG, "workspace smaller than dq_decode_gemv_nvfp4_workspace_size()");
+  }
+  return hip_status(dq::launch_gemv_nvfp4(x, B, view(W), out_kind, y, workspace, (hipStream_t)stream),
+                    "dq_decode_gemv_nvfp4");
+}
+
 dq_status dq_pack_mxfp4(const float* W, int64_t N, int64_t K, const dq_mxfp4_t* out, void* stream) {
   if (W == nullptr && N * K > 0) return fail(DQ_ERR_INVALID_ARG, "W is NULL");
   if (!aligned(W, 16)) return fail(DQ_ERR_INVALID_ARG, "W must be 16-byte aligned");
@@ -383,7 +415,8 @@ dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int ou
   dq_status st = check_lut(W, "W");
   if (st != DQ_OK) return st;
   if (B < 1 || B > 16) return fail(DQ_ERR_INVALID_ARG, "1 <= B <= 16 required");
-  if (x == nullptr || !aligned(x, 16)) return fail(DQ_ERR_INVALID_ARG, "x must be non-NULL and 16-byte aligned");
+  if ((x == nullptr && W->cols > 0) || !aligned(x, 16))
+    return fail(DQ_ERR_INVALID_ARG, "x must be 16-byte aligned and non-NULL unless K == 0");
   if (out_kind != DQ_OUT_F32 && out_kind != DQ_OUT_BF16) return fail(DQ_ERR_INVALID_ARG, "bad out_kind");
   if (y == nullptr && W->rows > 0) return fail(DQ_ERR_INVALID_ARG, "y is NULL");
   if (!aligned(y, 16)) return fail(DQ_ERR_INVALID_ARG, "y must be 16-byte aligned");

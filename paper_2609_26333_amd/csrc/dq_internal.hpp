@@ -97,6 +97,13 @@ inline int64_t gemm_column_split(int64_t M, int64_t N, int64_t bm, int64_t bn_fu
   return best * bn_full < N ? best * bn_full : N;
 }
 
+// NVFP4A16 decode GEMV (gemv_nvfp4.hip): bf16 x [B, K] times NVFP4 weights
+// [N, K].  ws: workspace of at least gemv_nvfp4_workspace_bytes(B, N, K)
+// bytes, or NULL to take it from the pool.
+size_t gemv_nvfp4_workspace_bytes(int64_t B, int64_t N, int64_t K);
+hipError_t launch_gemv_nvfp4(const uint16_t* x, int64_t B, const NvFp4View& w, int out_kind, void* y, void* ws,
+                             hipStream_t s);
+
 // a6: LUT GEMV (gemv.hip).  ws: workspace of at least
 // gemv_workspace_bytes(B, w) bytes, or NULL to take it from the pool.
 size_t gemv_workspace_bytes(int64_t B, const LutView& w);

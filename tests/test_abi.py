@@ -150,6 +150,16 @@ def test_invalid_arguments_rejected_on_host():
     assert lib.dq_decode_gemv_workspace_size(16, ctypes.byref(big), ctypes.byref(ws)) == dq.DQ_OK and ws.value > 0
     assert lib.dq_decode_gemv_workspace_size(17, ctypes.byref(big), ctypes.byref(ws)) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_decode_gemv(fake, 16, ctypes.byref(big), 0, fake, fake, ws.value - 16, None) == dq.DQ_ERR_INVALID_ARG
+    # NVFP4A16 GEMV: batch range, K % 16, short workspace
+    wn = _nv(7168, 5120, fake, fake, fake)
+    assert lib.dq_decode_gemv_nvfp4(fake, 0, ctypes.byref(wn), 0, fake, None, 0, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_decode_gemv_nvfp4(fake, 17, ctypes.byref(wn), 0, fake, None, 0, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_decode_gemv_nvfp4(fake, 1, ctypes.byref(_nv(16, 24, fake, fake, fake)), 0, fake, None, 0,
+                                    None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_decode_gemv_nvfp4(fake, 1, None, 0, fake, None, 0, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_decode_gemv_nvfp4_workspace_size(4, ctypes.byref(wn), ctypes.byref(ws)) == dq.DQ_OK and ws.value > 0
+    assert lib.dq_decode_gemv_nvfp4(fake, 4, ctypes.byref(wn), 0, fake, fake, ws.value - 16,
+                                    None) == dq.DQ_ERR_INVALID_ARG
     # PAPER_GRID without scales / G
     lw_p = dq._Lut(fake, fake, None, None, 16, 128, 3, 1)
     assert lib.dq_decode_gemv(fake, 1, ctypes.byref(lw_p), 0, fake, None, 0, None) == dq.DQ_ERR_INVALID_ARG

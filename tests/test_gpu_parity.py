@@ -375,3 +375,49 @@ def test_gemv_workspace_and_pool_paths_agree():
     assert torch.equal(y_ws, y_pool) and torch.equal(y_ws, y_ws2)
     codes_ref, lut_ref = lut.quantize_per_row(w, 3)
     assert linalg.rel_fro(host(y_ws), linalg.lut_gemv_per_row(xb, codes_ref, lut_ref)) <= TOL
+
+
+# ---------------------------------------------------------------- NVFP4A16 decode GEMV
+NV_GEMV_CASES = [(512, 512, 1), (100, 96, 3), (33, 1040, 2), (7168, 5120, 1), (5120, 17408, 1), (5120, 5120, 16),
+                 (12288, 4096, 4), (64, 4096, 8)]
+
+
+@pytest.mark.parametrize("N,K,B", NV_GEMV_CASES)
+def test_nvfp4a16_gemv(N, K, B):
+    """Weight-only NVFP4 decode: the GPU's own NVFP4 weight packing, bf16 x,
+    against the oracle's fp64 GEMV over the oracle-dequantized weights."""
+    say("nvfp4a16 gemv", N, K, B)
+    w = _lut_weight(N, K, 90)
+    qw, cw, Gw = nvfp4.quantize_dynamic(w)
+    Wq = dq.dq_pack_nvfp4(dev(w))
+    q_g, c_g, _, _ = L.nvfp4_unpack(host(Wq.codes), host(Wq.scales), N, K)
+    assert np.array_equal(q_g, qw) and np.array_equal(c_g, cw) and host(Wq.G)[0] == Gw
+    xb = synth.random_bf16(91 + B, (B, K), outlier_frac=0.005, outlier_factor=30)
+    ref = linalg.nvfp4a16_gemv(xb, qw, cw, Gw)
+    y = host(dq.dq_decode_gemv_nvfp4(bf16_dev(xb), Wq, out_kind=dq.OUT_F32))
+    err = linalg.rel_fro(y, ref)
+    say("  rel_fro", err)
+    assert err <= TOL
+    if K <= 5120:
+        yb = host(dq.dq_decode_gemv_nvfp4(bf16_dev(xb), Wq, out_kind=dq.OUT_BF16).float()).astype(np.float64)
+        assert linalg.rel_fro(yb, formats.bf16_rne_from_f64(ref)) <= TOL
+
+
+def test_nvfp4a16_gemv_empty_and_pool():
+    """K = 0 gives zeros; a NULL workspace (library pool) gives the same
+    result as a caller workspace."""
+    W0 = dq.NvFp4Tensor.empty(40, 0)
+    y0 = dq.dq_decode_gemv_nvfp4(torch.zeros((2, 0), dtype=torch.int16, device="cuda"), W0)
+    assert tuple(y0.shape) == (2, 40) and not host(y0).any()
+    N, K, B = 5120, 5120, 2
+    w = _lut_weight(N, K, 92)
+    Wq = dq.dq_pack_nvfp4(dev(w))
+    xb = synth.random_bf16(93, (B, K), outlier_frac=0.005, outlier_factor=30)
+    x = bf16_dev(xb)
+    assert dq.dq_decode_gemv_nvfp4_workspace_size(B, Wq) > 0
+    y_ws = dq.dq_decode_gemv_nvfp4(x, Wq)
+    y_pool = torch.empty_like(y_ws)
+    d = Wq.desc()
+    assert dq.lib().dq_decode_gemv_nvfp4(x.data_ptr(), B, ctypes.byref(d), dq.OUT_F32, y_pool.data_ptr(), None, 0,
+                                         torch.cuda.current_stream().cuda_stream) == dq.DQ_OK
+    assert torch.equal(y_ws, y_pool)

@@ -75,6 +75,32 @@ def test_gemv_per_row_lut_rational():
             assert abs(Fraction(float(y[b, n])) - sum(terms)) <= bound
 
 
+def test_nvfp4a16_gemv_rational():
+    """Weight-only NVFP4 GEMV against a loop over the format's definition:
+    E2M1 value table, E4M3 decode, global scale."""
+    rng = np.random.default_rng(35)
+    W = (rng.standard_normal((4, 48)) * 0.02).astype(np.float32)
+    q, c, G = nvfp4.quantize_dynamic(W)
+    x = bf16_bits_from_f32(rng.standard_normal((2, 48)).astype(np.float32))
+    y = linalg.nvfp4a16_gemv(x, q, c, G)
+    e2m1 = [Fraction(v) for v in ("0", "1/2", "1", "3/2", "2", "3", "4", "6")]
+
+    def e4m3(b):
+        e, m = (int(b) >> 3) & 0xF, int(b) & 7
+        return Fraction(m, 512) if e == 0 else Fraction(8 + m, 8) * Fraction(2) ** (e - 7)
+
+    xv = formats.f64_from_bf16_bits(x)
+    for b in range(2):
+        for n in range(4):
+            terms = []
+            for k in range(48):
+                code = int(q[n, k])
+                w = (-1 if code & 8 else 1) * e2m1[code & 7] * e4m3(c[n, k // 16]) * Fraction(float(G))
+                terms.append(Fraction(float(xv[b, k])) * w)
+            bound = sum(abs(t) for t in terms) * 48 * Fraction(1, 2 ** 53)
+            assert abs(Fraction(float(y[b, n])) - sum(terms)) <= bound
+
+
 def test_gemv_paper_grid_rational():
     rng = np.random.default_rng(34)
     W = (rng.standard_normal((3, 32)) * 0.02).astype(np.float32)
