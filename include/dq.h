@@ -124,7 +124,7 @@ typedef struct dq_lut {
 
 /*
  * MXFP4 tensor (OCP Microscaling: the W4A4 format the paper runs for models
- * released natively in MXFP4, Sec. 4).  Logical content: rows x cols E2M1
+ * released natively in MXFP4, Sec. 3.2).  Logical content: rows x cols E2M1
  * codes (as NVFP4) and one E8M0 scale code per 32 consecutive columns of a
  * row; element value = e2m1(code) * 2^(scale - 127).  No tensor scale.
  *
@@ -229,7 +229,7 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
                           void* stream);
 
 /* ---- NVFP4A16 decode GEMV ------------------------------------------------
- * The weight-only NVFP4 decode of format disaggregation (Sec. 3: decode
+ * The weight-only NVFP4 decode of format disaggregation (Sec. 2.3: decode
  * keeps 16-bit activations and quantizes only the weights; App. A "NVFP4"):
  * y[b, n] = sum_k x[b, k] * w_hat[n, k], w_hat = e2m1 * e4m3(scale) * G.
  * x: device bf16 [B, K] row-major, 1 <= B <= 16.  W: NVFP4 weights as packed
@@ -262,8 +262,9 @@ dq_status dq_prefill_gemm_mxfp4(const dq_mxfp4_t* A, const dq_mxfp4_t* W, int ou
                                 void* stream);
 
 /* ---- a6: weight-only LUT GEMV (decode; no activation quantization) -------
- * The weight-only path the paper serves decode with (Sec. 3 "Format
- * disaggregation"; time set by the weight bytes streamed per token, Sec. 5).
+ * The weight-only path the paper serves decode with (Sec. 2.3, format
+ * disaggregation; time set by the weight bytes streamed per token, App. C
+ * "Kernel specification").
  * y[b, n] = sum_k x[b, k] * w_hat[n, k], fp32 accumulation.
  * x: device bf16 [B, K] row-major, 1 <= B <= 16.  W: packed LUT weight.
  * out_kind DQ_OUT_F32 / DQ_OUT_BF16: y is device [B, N] row-major.

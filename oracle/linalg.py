@@ -48,7 +48,7 @@ def lut_gemv_paper(x_bits, codes, scale_bytes, G, grid) -> np.ndarray:
 
 
 def nvfp4a16_gemv(x_bits, codes, scale_codes, G) -> np.ndarray:
-    """Weight-only NVFP4 decode (Sec. 3, format disaggregation: 16-bit
+    """Weight-only NVFP4 decode (Sec. 2.3, format disaggregation: 16-bit
     activations, NVFP4 weights): ``y[b, n] = sum_k x[b, k] * w_hat[n, k]`` with
     the NVFP4 dequantization of App. A, in fp64."""
     return gemv_bf16(x_bits, nvfp4.dequantize(codes, scale_codes, G))

@@ -1,7 +1,7 @@
 """MXFP4 quantization (oracle; test infrastructure).
 
 The paper runs MXFP4 instead of NVFP4 for a model that is released natively
-in that format (Sec. 4, the accuracy table's footnote and the description of
+in that format (Sec. 3.2, the accuracy table's footnote, and the description of
 the evaluation arms) and does not restate the format.  This follows the OCP
 Microscaling Formats (MX) specification v1.0:
 

@@ -1,6 +1,6 @@
 // NVFP4A16 decode GEMV on gfx950: the weight-only NVFP4 decode of format
-// disaggregation (paper Sec. 3: decode keeps the activations in 16 bits and
-// only the weights quantized; App. A "NVFP4").
+// disaggregation (paper Sec. 2.3: decode keeps the activations in 16 bits
+// and only the weights quantized; App. A "Quantization formats", "NVFP4").
 //
 //   y[b, n] = G * sum_k x[b, k] * e2m1(c[n, k]) * e4m3(s[n, k/16])
 //

@@ -2,7 +2,8 @@
 // activations) and the block-scaled GEMM.
 //
 // The paper runs MXFP4 in place of NVFP4 for a model released natively in
-// that format (Sec. 4, the accuracy table and the evaluation arms).  The
+// that format (Sec. 3.2, the accuracy table of large LLMs, and its quantized
+// arms).  The
 // format is the OCP Microscaling one: E2M1 elements, one E8M0 (power-of-two)
 // scale per 32 consecutive elements along K, no tensor scale.
 //
