@@ -316,6 +316,15 @@ def main():
     torch.cuda.synchronize()
     t_pack_lut = e0.elapsed_time(e1)
     del W_dev
+    # LUT -> NVFP4 autocast of the packed LUT3 weight (the prefill view of a LUT model), once warm
+    dq.dq_autocast_lut_to_nvfp4(Wl)
+    torch.cuda.synchronize()
+    e0.record()
+    Wac = dq.dq_autocast_lut_to_nvfp4(Wl)
+    e1.record()
+    torch.cuda.synchronize()
+    t_autocast = e0.elapsed_time(e1)
+    del Wac
 
     # static activation scale from a calibration batch (running-max observer stand-in)
     A_cal = dq.dq_quantize_act_nvfp4(dev(calib.view(np.int16)))
@@ -426,7 +435,7 @@ def main():
                     "frac_fp4_peak": gemm_tflops / PEAK_FP4_TFLOPS,
                     "linear_TFLOP/s_incl_quant": prefill_tflops},
         "decode": decode,
-        "pack_ms": {"nvfp4": t_pack_nvfp4, "lut3_per_row": t_pack_lut},
+        "pack_ms": {"nvfp4": t_pack_nvfp4, "lut3_per_row": t_pack_lut, "lut3_to_nvfp4_autocast": t_autocast},
         "roofline": {"bound": "mfma", "kernel": "nvfp4_gemm_kernel (the launches of one dq_prefill_gemm call)",
                      "achieved": gemm_tflops,
                      "peak": PEAK_FP16_TFLOPS, "unit": "TFLOP/s", "frac": gemm_tflops / PEAK_FP16_TFLOPS,

@@ -11,8 +11,8 @@
  *   - Buffers are device memory owned by the caller.  The library keeps no
  *     state except a thread-local last-error string and a per-device memory
  *     pool, from which it takes stream-ordered staging only for
- *     dq_prefill_gemm's fused path and for dq_decode_gemv called without a
- *     workspace.
+ *     dq_prefill_gemm's fused path, dq_autocast_lut_to_nvfp4, and the GEMVs
+ *     called without a workspace.
  *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*;
  *     NULL is the default stream).  Nothing synchronizes inside the library.
  *   - Arguments are validated on the host before any HIP call; a rejected
@@ -227,6 +227,17 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
                           const dq_nvfp4_t* W, int64_t M, int out_kind, void* Y,
                           const float* G_out_static, const dq_nvfp4_t* Yq, int epilogue_flags,
                           void* stream);
+
+/* ---- LUT -> NVFP4 autocast ----------------------------------------------
+ * The re-quantization of LUT weights to NVFP4 for native low-precision
+ * prefill (Sec. 2.3: "autocast").  The dequantized LUT weight (PER_ROW: the
+ * fp16 table entry; PAPER_GRID: fp32(grid * e4m3) * G, one rounding) is
+ * packed by the NVFP4 weight rule of dq_pack_nvfp4 (G = amax / 2688 unless
+ * G_override is given).  out: rows, cols as W.  The fp32 staging copy of the
+ * weight (rows * cols * 4 bytes) is taken from the library's pool,
+ * stream-ordered. */
+dq_status dq_autocast_lut_to_nvfp4(const dq_lut_t* W, const float* G_override, const dq_nvfp4_t* out,
+                                   void* stream);
 
 /* ---- NVFP4A16 decode GEMV ------------------------------------------------
  * The weight-only NVFP4 decode of format disaggregation (Sec. 2.3: decode

@@ -43,7 +43,7 @@ from typing import Tuple
 
 import numpy as np
 
-from . import formats
+from . import formats, nvfp4
 
 PER_ROW = 0
 PAPER_GRID = 1
@@ -142,3 +142,19 @@ def dequantize_paper_grid(codes, scale_bytes, G, grid) -> np.ndarray:
     v = g[c].reshape(N, K // 16, 16)
     d = formats.e4m3_decode(scale_bytes)[..., None]
     return (v * d * np.float64(np.float32(G))).reshape(N, K)
+
+
+# ---------------------------------------------------------------- autocast
+def autocast_to_nvfp4(w_hat, G=None):
+    """LUT -> NVFP4 autocast (Sec. 2.3: the LUT weights are re-quantized to
+    NVFP4 for native low-precision prefill).  ``w_hat`` is the dequantized LUT
+    weight (fp64, exact); it is rounded once to fp32 (exact for PER_ROW
+    tables, one rounding of an exact product for PAPER_GRID) and quantized by
+    the NVFP4 weight rule of App. A: ``G = amax / 2688`` unless given.
+
+    Returns ``(codes, scale_codes, G)``."""
+    w32 = np.asarray(w_hat, dtype=np.float64).astype(np.float32)
+    if G is None:
+        return nvfp4.quantize_dynamic(w32)
+    q, c = nvfp4.quantize(w32, np.float32(G))
+    return q, c, np.float32(G)

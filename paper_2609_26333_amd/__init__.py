@@ -67,6 +67,7 @@ def _load() -> ctypes.CDLL:
         "dq_quantize_act_nvfp4": (S, [P, I64, I64, P, ctypes.POINTER(_NvFp4), P]),
         "dq_prefill_gemm": (S, [ctypes.POINTER(_NvFp4), P, P, ctypes.POINTER(_NvFp4), I64, I32, P, P,
                                 ctypes.POINTER(_NvFp4), I32, P]),
+        "dq_autocast_lut_to_nvfp4": (S, [ctypes.POINTER(_Lut), P, ctypes.POINTER(_NvFp4), P]),
         "dq_decode_gemv_nvfp4_workspace_size": (S, [I64, ctypes.POINTER(_NvFp4), SZ]),
         "dq_decode_gemv_nvfp4": (S, [P, I64, ctypes.POINTER(_NvFp4), I32, P, P, ctypes.c_size_t, P]),
         "dq_mxfp4_sizes": (S, [I64, I64, SZ, SZ]),
@@ -88,7 +89,7 @@ EXPORTED = ("dq_abi_version", "dq_status_string", "dq_last_error", "dq_nvfp4_siz
             "dq_pack_nvfp4", "dq_pack_lut3", "dq_quantize_act_nvfp4", "dq_prefill_gemm",
             "dq_decode_gemv_workspace_size", "dq_decode_gemv", "dq_mxfp4_sizes", "dq_pack_mxfp4",
             "dq_quantize_act_mxfp4", "dq_prefill_gemm_mxfp4", "dq_decode_gemv_nvfp4_workspace_size",
-            "dq_decode_gemv_nvfp4")
+            "dq_decode_gemv_nvfp4", "dq_autocast_lut_to_nvfp4")
 
 
 def lib() -> ctypes.CDLL:
@@ -272,6 +273,15 @@ def dq_prefill_gemm(W: NvFp4Tensor, A: Optional[NvFp4Tensor] = None, X: Optional
                                 ctypes.byref(dyq) if dyq is not None else None, epilogue_flags, _stream(stream)),
            "dq_prefill_gemm")
     return Yq if out_kind == OUT_NVFP4 else Y
+
+
+def dq_autocast_lut_to_nvfp4(W: LutWeight, G_override: Optional[torch.Tensor] = None,
+                             out: Optional[NvFp4Tensor] = None, stream=None) -> NvFp4Tensor:
+    out = NvFp4Tensor.empty(W.rows, W.cols, W.codes.device) if out is None else out
+    dw, do = W.desc(), out.desc()
+    _check(_lib.dq_autocast_lut_to_nvfp4(ctypes.byref(dw), _ptr(G_override), ctypes.byref(do), _stream(stream)),
+           "dq_autocast_lut_to_nvfp4")
+    return out
 
 
 def dq_pack_mxfp4(W: torch.Tensor, out: Optional[MxFp4Tensor] = None, stream=None) -> MxFp4Tensor:

@@ -238,6 +238,17 @@ dq_status dq_pack_lut3(const float* W, int64_t N, int64_t K, int bits, int mode,
   return hip_status(dq::launch_pack_lut(W, N, K, grid, view(out), (hipStream_t)stream), "dq_pack_lut3");
 }
 
+dq_status dq_autocast_lut_to_nvfp4(const dq_lut_t* W, const float* G_override, const dq_nvfp4_t* out,
+                                   void* stream) {
+  dq_status st = check_lut(W, "W");
+  if (st != DQ_OK) return st;
+  if (G_override != nullptr && !aligned(G_override, 4)) return fail(DQ_ERR_INVALID_ARG, "G_override misaligned");
+  st = check_nvfp4(out, "out", W->rows, W->cols);
+  if (st != DQ_OK) return st;
+  return hip_status(dq::launch_autocast_lut(view(W), G_override, view(out), (hipStream_t)stream),
+                    "dq_autocast_lut_to_nvfp4");
+}
+
 dq_status dq_quantize_act_nvfp4(const uint16_t* X, int64_t M, int64_t K, const float* G_static,
                                 const dq_nvfp4_t* out, void* stream) {
   if (X == nullptr && M * K > 0) return fail(DQ_ERR_INVALID_ARG, "X is NULL");

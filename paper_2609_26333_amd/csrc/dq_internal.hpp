@@ -33,6 +33,10 @@ hipError_t launch_pack_nvfp4(const float* W, int64_t N, int64_t K, const float* 
 hipError_t launch_pack_lut(const float* W, int64_t N, int64_t K, const uint16_t* grid_host,
                            const LutView& out, hipStream_t s);
 
+// LUT -> NVFP4 autocast (pack_lut.hip): dequantize to a pooled fp32
+// staging copy, then the NVFP4 weight packing
+hipError_t launch_autocast_lut(const LutView& w, const float* G_override, const NvFp4View& out, hipStream_t s);
+
 // a3 / a4: NVFP4 GEMM (gemm.hip)
 struct GemmArgs {
   NvFp4View A;            // valid when X == nullptr

@@ -274,6 +274,62 @@ __global__ __launch_bounds__(256) void amax_f32_kernel(const float* __restrict__
   if (threadIdx.x == 0) atomic_max_nonneg(out, fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3])));
 }
 
+
+// ---------------------------------------------------------------- autocast
+// LUT -> NVFP4 autocast, step 1: the dequantized LUT weight as fp32 [N, K],
+// one thread per 32-code group of the tiled layout (dq.h).  PER_ROW entries
+// are fp16 (exact in fp32); a PAPER_GRID value grid * e4m3 * G is computed
+// as fp32(grid * e4m3) (exact: at most 15 significant bits) times G, one
+// rounding of the exact product.
+template <int BITS, int MODE>
+__global__ __launch_bounds__(256) void lut_dequant_kernel(const uint8_t* __restrict__ codes,
+                                                          const uint16_t* __restrict__ lut,
+                                                          const uint8_t* __restrict__ scales,
+                                                          const float* __restrict__ Gp, int64_t N, int64_t K,
+                                                          int64_t tiles_c, float* __restrict__ out) {
+  constexpr int GB = BITS == 3 ? 12 : 8;   // bytes per 32-code group
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t tile = gid >> 6;
+  const int g = (int)(gid & 63), i = g & 15, q = g >> 4;
+  const int64_t tr = tile / tiles_c, c = tile - tr * tiles_c;
+  const int64_t row = tr * 16 + i, col0 = c * 128 + q * 32;
+  if (row >= N || col0 >= K) return;
+  const uint8_t* gp = codes + tile * 64 * GB + g * GB;
+  uint32_t d[3];
+  d[0] = *reinterpret_cast<const uint32_t*>(gp);
+  d[1] = *reinterpret_cast<const uint32_t*>(gp + 4);
+  d[2] = BITS == 3 ? *reinterpret_cast<const uint32_t*>(gp + 8) : 0u;
+  float sb[2] = {1.0f, 1.0f};
+  float G = 1.0f;
+  if (MODE == 1) {
+    sb[0] = e4m3_decode(scales[tile * 128 + g * 2]);
+    sb[1] = e4m3_decode(scales[tile * 128 + g * 2 + 1]);
+    G = *Gp;
+  }
+  float* o = out + row * K + col0;
+#pragma unroll
+  for (int t = 0; t < 32; ++t) {
+    const int sl = t >> 2, b = t & 3;
+    uint32_t code;
+    if (BITS == 3) {
+      if (sl < 6)
+        code = (d[sl >> 1] >> (8 * b + 3 * (sl & 1))) & 7u;
+      else
+        code = ((d[sl - 6] >> (8 * b + 6)) & 3u) | (((d[2] >> (8 * b + 6 + (sl - 6))) & 1u) << 2);
+    } else {
+      code = (d[sl >> 2] >> (8 * b + 2 * (sl & 3))) & 3u;
+    }
+    const uint16_t e = MODE == 0 ? lut[row * (1 << BITS) + code] : lut[code];
+    const float v = (float)__builtin_bit_cast(_Float16, e);
+    if (MODE == 0) {
+      o[t] = v;
+    } else {
+      const float p = v * sb[t >> 4];   // exact
+      o[t] = p * G;
+    }
+  }
+}
+
 }  // namespace
 
 // paper grids (App. A "LUT formats") rounded to fp16
@@ -320,6 +376,31 @@ hipError_t launch_pack_lut(const float* W, int64_t N, int64_t K, const uint16_t*
     hipLaunchKernelGGL(pack_lut_paper_kernel<2>, dim3((unsigned)blocks), dim3(256), 0, s, W, N, N16, K, KC, out.G, g,
                        zl, out.codes, out.scales, out.lut);
   return hipGetLastError();
+}
+
+hipError_t launch_autocast_lut(const LutView& w, const float* G_override, const NvFp4View& out, hipStream_t s) {
+  const int64_t N = w.rows, K = w.cols;
+  float* tmp = nullptr;
+  hipError_t e = hipSuccess;
+  if (N * K > 0) {
+    e = pool_alloc_async(reinterpret_cast<void**>(&tmp), (size_t)(N * K) * 4, s);
+    if (e != hipSuccess) return e;
+    const int64_t tiles_c = (K + 127) / 128;
+    const int64_t threads = (N + 15) / 16 * tiles_c * 64;
+    typedef void (*kern_t)(const uint8_t*, const uint16_t*, const uint8_t*, const float*, int64_t, int64_t, int64_t,
+                           float*);
+    const kern_t kern = w.bits == 3 ? (w.mode == 0 ? lut_dequant_kernel<3, 0> : lut_dequant_kernel<3, 1>)
+                                    : (w.mode == 0 ? lut_dequant_kernel<2, 0> : lut_dequant_kernel<2, 1>);
+    hipLaunchKernelGGL(kern, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, w.codes, w.lut, w.scales, w.G,
+                       N, K, tiles_c, tmp);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess) e = launch_pack_nvfp4(tmp, N, K, G_override, out, s);
+  if (tmp != nullptr) {
+    const hipError_t f = hipFreeAsync(tmp, s);
+    if (e == hipSuccess) e = f;
+  }
+  return e;
 }
 
 }  // namespace dq

@@ -160,6 +160,11 @@ def test_invalid_arguments_rejected_on_host():
     assert lib.dq_decode_gemv_nvfp4_workspace_size(4, ctypes.byref(wn), ctypes.byref(ws)) == dq.DQ_OK and ws.value > 0
     assert lib.dq_decode_gemv_nvfp4(fake, 4, ctypes.byref(wn), 0, fake, fake, ws.value - 16,
                                     None) == dq.DQ_ERR_INVALID_ARG
+    # autocast: output shape must match W
+    assert lib.dq_autocast_lut_to_nvfp4(ctypes.byref(lw), None, ctypes.byref(_nv(16, 64, fake, fake, fake)),
+                                        None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_autocast_lut_to_nvfp4(None, None, ctypes.byref(_nv(16, 128, fake, fake, fake)),
+                                        None) == dq.DQ_ERR_INVALID_ARG
     # PAPER_GRID without scales / G
     lw_p = dq._Lut(fake, fake, None, None, 16, 128, 3, 1)
     assert lib.dq_decode_gemv(fake, 1, ctypes.byref(lw_p), 0, fake, None, 0, None) == dq.DQ_ERR_INVALID_ARG

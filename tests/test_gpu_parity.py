@@ -421,3 +421,46 @@ def test_nvfp4a16_gemv_empty_and_pool():
     assert dq.lib().dq_decode_gemv_nvfp4(x.data_ptr(), B, ctypes.byref(d), dq.OUT_F32, y_pool.data_ptr(), None, 0,
                                          torch.cuda.current_stream().cuda_stream) == dq.DQ_OK
     assert torch.equal(y_ws, y_pool)
+
+
+# ---------------------------------------------------------------- LUT -> NVFP4 autocast
+@pytest.mark.parametrize("N,K,bits,mode", [(512, 512, 3, 0), (20, 96, 3, 0), (300, 1024, 2, 0), (12288, 4096, 3, 0),
+                                           (37, 1024, 3, 1), (64, 4096, 2, 1)])
+def test_lut_autocast_to_nvfp4(N, K, bits, mode):
+    """The GPU's own LUT packing, re-quantized to NVFP4 on the GPU, against
+    the oracle's autocast of the oracle's LUT weight: codes, scales and G
+    bit-exact; then the prefill GEMM on the autocast weights."""
+    say("autocast", N, K, bits, mode)
+    w = _lut_weight(N, K, 100 + bits)
+    if mode == dq.LUT_PER_ROW:
+        codes_ref, table = lut.quantize_per_row(w, bits)
+        w_hat = lut.dequantize_per_row(codes_ref, table)
+    else:
+        grid = lut.default_grid(bits)
+        codes_ref, sb, G_l = lut.quantize_paper_grid(w, grid)
+        w_hat = lut.dequantize_paper_grid(codes_ref, sb, G_l, grid)
+    q_ref, c_ref, G_ref = lut.autocast_to_nvfp4(w_hat)
+    Wl = dq.dq_pack_lut3(dev(w), bits=bits, mode=mode)
+    Wn = dq.dq_autocast_lut_to_nvfp4(Wl)
+    q, c, qfull, cfull = L.nvfp4_unpack(host(Wn.codes), host(Wn.scales), N, K)
+    assert host(Wn.G)[0] == G_ref
+    assert np.array_equal(c, c_ref), f"scales differ at {np.argwhere(c != c_ref)[:5]}"
+    assert np.array_equal(q, q_ref), f"codes differ at {np.argwhere(q != q_ref)[:5]}"
+    assert not qfull[N:].any() and not cfull[N:].any()
+    if N * K <= 1 << 22:
+        xb = synth.random_bf16(110, (64, K), outlier_frac=0.01, outlier_factor=20)
+        qa, ca, Ga = nvfp4.quantize_bf16_activations(xb)
+        A = _upload_nvfp4(qa, ca, Ga)
+        y = host(dq.dq_prefill_gemm(Wn, A=A, out_kind=dq.OUT_F32))
+        assert linalg.rel_fro(y, linalg.nvfp4_gemm(qa, ca, Ga, q_ref, c_ref, G_ref)) <= TOL
+
+
+def test_lut_autocast_static_scale():
+    w = _lut_weight(48, 256, 111)
+    Wl = dq.dq_pack_lut3(dev(w), bits=3)
+    G = np.float32(3.0e-4)
+    Wn = dq.dq_autocast_lut_to_nvfp4(Wl, G_override=dev(np.array([G], np.float32)))
+    codes_ref, table = lut.quantize_per_row(w, 3)
+    q_ref, c_ref, _ = lut.autocast_to_nvfp4(lut.dequantize_per_row(codes_ref, table), G=G)
+    q, c, _, _ = L.nvfp4_unpack(host(Wn.codes), host(Wn.scales), 48, 256)
+    assert host(Wn.G)[0] == G and np.array_equal(q, q_ref) and np.array_equal(c, c_ref)

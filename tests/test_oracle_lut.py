@@ -14,7 +14,7 @@ from fractions import Fraction
 import numpy as np
 import pytest
 
-from oracle import formats, lut
+from oracle import formats, lut, nvfp4
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -171,3 +171,37 @@ def test_printed_lut3_grid_is_a_constrained_lloyd_max_fixed_point():
             if not fixed[j]:
                 g[j] = y[idx == j].mean()
     assert np.max(np.abs(g - np.array(_printed_grids()["LUT3"]))) < 0.02
+
+
+def test_autocast_reproduces_nvfp4_exact_tables():
+    """LUT entries that NVFP4 represents exactly come back unchanged: every
+    16-block holds the tensor's largest entry 6c with c = 7/256, so
+    G = 6c/2688 = 2^-14 exactly, the block scale codes to 448 = 6c / (6G),
+    S = 448 G = c, and each entry e*c (e an E2M1 magnitude) is a code."""
+    rng = np.random.default_rng(50)
+    c = np.float16(7.0 / 256.0)
+    e2m1 = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+    N, K = 6, 64
+    table = np.zeros((N, 8), np.float16)
+    for n in range(N):
+        vals = np.sort(rng.choice(e2m1[:-1], 7, replace=True))
+        table[n] = (np.concatenate([vals, [6.0]]) * np.float64(c)).astype(np.float16)
+    codes = rng.integers(0, 8, (N, K)).astype(np.uint8)
+    codes[:, ::16] = 7                                    # the largest entry in every block
+    w_hat = lut.dequantize_per_row(codes, table)
+    q, sc, G = lut.autocast_to_nvfp4(w_hat)
+    assert G == np.float32(2.0 ** -14)
+    assert np.all(sc == 0x7E)
+    assert np.array_equal(nvfp4.dequantize(q, sc, G), w_hat)
+
+
+def test_autocast_paper_grid_is_one_rounding():
+    """PAPER_GRID entries grid * e4m3 * G are exact in fp64 and rounded once to
+    fp32 before the NVFP4 rule; a given G is passed through."""
+    W = (np.random.default_rng(51).standard_normal((8, 64)) * 0.02).astype(np.float32)
+    grid = lut.default_grid(3)
+    codes, sb, G = lut.quantize_paper_grid(W, grid)
+    w_hat = lut.dequantize_paper_grid(codes, sb, G, grid)
+    q, c, G2 = lut.autocast_to_nvfp4(w_hat, G=np.float32(0.001))
+    q_ref, c_ref = nvfp4.quantize(w_hat.astype(np.float32), np.float32(0.001))
+    assert G2 == np.float32(0.001) and np.array_equal(q, q_ref) and np.array_equal(c, c_ref)
