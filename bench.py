@@ -403,6 +403,17 @@ def main():
         return ea.elapsed_time(eb) / reps
 
     per = {"quant": back_to_back(lambda i: quant(i)), "gemm": back_to_back(lambda i: gemm())}
+    # the same quantizer fused with the RMSNorm that precedes the projection
+    gamma = dev(synth.bf16_bits_from_f32((1.0 + 0.2 * synth.random_f32(7, (1, K))).astype(np.float32))[0]
+                .view(np.int16))
+
+    norm_ws = torch.empty(4 * M, dtype=torch.uint8, device="cuda")
+
+    def norm_quant(i):
+        return lib.dq_rmsnorm_quantize_act_nvfp4(ctypes.c_void_p(Xs[i % n_x].data_ptr()),
+                                                 ctypes.c_void_p(gamma.data_ptr()), ctypes.c_float(1e-6), M, K, gx,
+                                                 ctypes.byref(dA), ctypes.c_void_p(norm_ws.data_ptr()), 4 * M, sp)
+    per["norm_quant"] = back_to_back(norm_quant)
     for b in Bs:
         per[f"gemv_b{b}"] = back_to_back(lambda i, b=b: gemv(i, b))
 
@@ -430,6 +441,7 @@ def main():
                    "M": M, "N": N, "K": K, "decode_batches": list(Bs), "static_G_x": G_x_host,
                    "decode_weight_copies": n_w, "x_copies": n_x},
         "prefill": {"quant_us": per["quant"] * 1e3, "quant_GB/s": quant_bytes / (per["quant"] * 1e-3) / 1e9,
+                    "rmsnorm_quant_us": per["norm_quant"] * 1e3,
                     "gemm_us": per["gemm"] * 1e3, "gemm_TFLOP/s": gemm_tflops,
                     "frac_fp16_mfma_peak": gemm_tflops / PEAK_FP16_TFLOPS,
                     "frac_fp4_peak": gemm_tflops / PEAK_FP4_TFLOPS,

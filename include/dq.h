@@ -11,8 +11,9 @@
  *   - Buffers are device memory owned by the caller.  The library keeps no
  *     state except a thread-local last-error string and a per-device memory
  *     pool, from which it takes stream-ordered staging only for
- *     dq_prefill_gemm's fused path, dq_autocast_lut_to_nvfp4, and the GEMVs
- *     called without a workspace.
+ *     dq_prefill_gemm's fused path, dq_autocast_lut_to_nvfp4, and the
+ *     calls that take a workspace (the GEMVs, the fused RMSNorm quantizer)
+ *     when they are given none.
  *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*;
  *     NULL is the default stream).  Nothing synchronizes inside the library.
  *   - Arguments are validated on the host before any HIP call; a rejected
@@ -227,6 +228,21 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
                           const dq_nvfp4_t* W, int64_t M, int out_kind, void* Y,
                           const float* G_out_static, const dq_nvfp4_t* Yq, int epilogue_flags,
                           void* stream);
+
+/* ---- RMSNorm fused with the NVFP4 activation quantizer -------------------
+ * The paper quantizes activations inside the normalization that feeds the
+ * quantized projections (App. C, "Prefill measurements").  Per row of the
+ * bf16 X [M, K]: ss = sum of x^2 (fp64), ms = fp32(ss / K),
+ * inv = fp32(1 / fp32(sqrt(fp32(ms + eps)))), y = fp32(fp32(x * inv) * gamma)
+ * with gamma device bf16 [K] (16-byte aligned); y is then quantized by the
+ * a1 rule of dq_quantize_act_nvfp4 (G_static, or G = amax(y) / 2688 when
+ * NULL).  out: rows = M, cols = K.  workspace: device memory of at least
+ * 4 M bytes (16-byte aligned) for the per-row statistics, not in use by
+ * other work during the call; NULL takes it from the library's pool,
+ * stream-ordered.  eps must be finite, >= 0. */
+dq_status dq_rmsnorm_quantize_act_nvfp4(const uint16_t* X, const uint16_t* gamma, float eps, int64_t M,
+                                        int64_t K, const float* G_static, const dq_nvfp4_t* out,
+                                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---- LUT -> NVFP4 autocast ----------------------------------------------
  * The re-quantization of LUT weights to NVFP4 for native low-precision

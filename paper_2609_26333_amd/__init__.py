@@ -68,6 +68,8 @@ def _load() -> ctypes.CDLL:
         "dq_prefill_gemm": (S, [ctypes.POINTER(_NvFp4), P, P, ctypes.POINTER(_NvFp4), I64, I32, P, P,
                                 ctypes.POINTER(_NvFp4), I32, P]),
         "dq_autocast_lut_to_nvfp4": (S, [ctypes.POINTER(_Lut), P, ctypes.POINTER(_NvFp4), P]),
+        "dq_rmsnorm_quantize_act_nvfp4": (S, [P, P, ctypes.c_float, I64, I64, P, ctypes.POINTER(_NvFp4), P,
+                                              ctypes.c_size_t, P]),
         "dq_decode_gemv_nvfp4_workspace_size": (S, [I64, ctypes.POINTER(_NvFp4), SZ]),
         "dq_decode_gemv_nvfp4": (S, [P, I64, ctypes.POINTER(_NvFp4), I32, P, P, ctypes.c_size_t, P]),
         "dq_mxfp4_sizes": (S, [I64, I64, SZ, SZ]),
@@ -89,7 +91,7 @@ EXPORTED = ("dq_abi_version", "dq_status_string", "dq_last_error", "dq_nvfp4_siz
             "dq_pack_nvfp4", "dq_pack_lut3", "dq_quantize_act_nvfp4", "dq_prefill_gemm",
             "dq_decode_gemv_workspace_size", "dq_decode_gemv", "dq_mxfp4_sizes", "dq_pack_mxfp4",
             "dq_quantize_act_mxfp4", "dq_prefill_gemm_mxfp4", "dq_decode_gemv_nvfp4_workspace_size",
-            "dq_decode_gemv_nvfp4", "dq_autocast_lut_to_nvfp4")
+            "dq_decode_gemv_nvfp4", "dq_autocast_lut_to_nvfp4", "dq_rmsnorm_quantize_act_nvfp4")
 
 
 def lib() -> ctypes.CDLL:
@@ -273,6 +275,22 @@ def dq_prefill_gemm(W: NvFp4Tensor, A: Optional[NvFp4Tensor] = None, X: Optional
                                 ctypes.byref(dyq) if dyq is not None else None, epilogue_flags, _stream(stream)),
            "dq_prefill_gemm")
     return Yq if out_kind == OUT_NVFP4 else Y
+
+
+def dq_rmsnorm_quantize_act_nvfp4(X: torch.Tensor, gamma: torch.Tensor, eps: float = 1e-6,
+                                  G_static: Optional[torch.Tensor] = None, out: Optional[NvFp4Tensor] = None,
+                                  stream=None) -> NvFp4Tensor:
+    X, gamma = _as_u16(X), _as_u16(gamma)
+    assert X.is_contiguous() and X.dim() == 2 and gamma.is_contiguous() and gamma.numel() == X.shape[1]
+    M, K = X.shape
+    out = NvFp4Tensor.empty(M, K, X.device) if out is None else out
+    d = out.desc()
+    ws = torch.empty(max(4 * M, 16), dtype=torch.uint8, device=X.device)   # per-row statistics
+    _check(_lib.dq_rmsnorm_quantize_act_nvfp4(X.data_ptr() if X.numel() else None,
+                                              gamma.data_ptr() if gamma.numel() else None, eps, M, K,
+                                              _ptr(G_static), ctypes.byref(d), ws.data_ptr(), ws.numel(),
+                                              _stream(stream)), "dq_rmsnorm_quantize_act_nvfp4")
+    return out
 
 
 def dq_autocast_lut_to_nvfp4(W: LutWeight, G_override: Optional[torch.Tensor] = None,

@@ -238,6 +238,24 @@ dq_status dq_pack_lut3(const float* W, int64_t N, int64_t K, int bits, int mode,
   return hip_status(dq::launch_pack_lut(W, N, K, grid, view(out), (hipStream_t)stream), "dq_pack_lut3");
 }
 
+dq_status dq_rmsnorm_quantize_act_nvfp4(const uint16_t* X, const uint16_t* gamma, float eps, int64_t M, int64_t K,
+                                        const float* G_static, const dq_nvfp4_t* out, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  if (M < 0 || K < 0 || K % 16 != 0) return fail(DQ_ERR_INVALID_ARG, "M >= 0, K >= 0, K %% 16 == 0 required");
+  if ((X == nullptr && M * K > 0) || !aligned(X, 16)) return fail(DQ_ERR_INVALID_ARG, "X must be 16-byte aligned");
+  if ((gamma == nullptr && K > 0) || !aligned(gamma, 16))
+    return fail(DQ_ERR_INVALID_ARG, "gamma must be 16-byte aligned");
+  if (!(eps >= 0.0f) || eps > 3.0e38f) return fail(DQ_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  if (G_static != nullptr && !aligned(G_static, 4)) return fail(DQ_ERR_INVALID_ARG, "G_static misaligned");
+  if (workspace != nullptr && (!aligned(workspace, 16) || workspace_bytes < (size_t)M * 4))
+    return fail(DQ_ERR_INVALID_ARG, "workspace must be 16-byte aligned and hold 4 M bytes");
+  dq_status st = check_nvfp4(out, "out", M, K);
+  if (st != DQ_OK) return st;
+  return hip_status(dq::launch_rmsnorm_quantize_act(X, gamma, eps, M, K, G_static, view(out), workspace,
+                                                    (hipStream_t)stream),
+                    "dq_rmsnorm_quantize_act_nvfp4");
+}
+
 dq_status dq_autocast_lut_to_nvfp4(const dq_lut_t* W, const float* G_override, const dq_nvfp4_t* out,
                                    void* stream) {
   dq_status st = check_lut(W, "W");

@@ -33,6 +33,13 @@ hipError_t launch_pack_nvfp4(const float* W, int64_t N, int64_t K, const float* 
 hipError_t launch_pack_lut(const float* W, int64_t N, int64_t K, const uint16_t* grid_host,
                            const LutView& out, hipStream_t s);
 
+// RMSNorm fused with the NVFP4 activation quantizer (quant.hip): per-row
+// statistics into the workspace ws (4 M bytes; NULL: pooled staging), then
+// the tile quantizer on the normalized values; G_static == nullptr takes G
+// from the normalized tensor's amax
+hipError_t launch_rmsnorm_quantize_act(const uint16_t* X, const uint16_t* gamma, float eps, int64_t M, int64_t K,
+                                       const float* G_static, const NvFp4View& out, void* ws, hipStream_t s);
+
 // LUT -> NVFP4 autocast (pack_lut.hip): dequantize to a pooled fp32
 // staging copy, then the NVFP4 weight packing
 hipError_t launch_autocast_lut(const LutView& w, const float* G_override, const NvFp4View& out, hipStream_t s);

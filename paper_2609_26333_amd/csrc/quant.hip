@@ -129,14 +129,16 @@ __device__ inline uint32_t quantize8(const float (&v)[8], float G, uint32_t& sca
   return fp4_canonical_zero(w);
 }
 
-// One wavefront per 32x64 tile; 4 wavefronts per block.
-template <typename T>
+// One wavefront per 32x64 tile; 4 wavefronts per block.  With NORM the
+// loaded values are RMSNorm-ed first: fp32(fp32(x * inv[row]) * gamma[col]).
+template <typename T, bool NORM = false>
 __global__ __launch_bounds__(256) void quantize_tiles_kernel(const T* __restrict__ x, int64_t rows,
                                                              int64_t cols, const float* __restrict__ Gp,
                                                              uint8_t* __restrict__ codes,
                                                              uint8_t* __restrict__ scales,
                                                              int64_t tiles_r, int64_t tiles_c,
-                                                             float* G_out) {
+                                                             float* G_out, const float* __restrict__ inv = nullptr,
+                                                             const uint16_t* __restrict__ gamma = nullptr) {
   const int lane = threadIdx.x & 63;
   const int64_t tile = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const float G = *Gp;
@@ -154,10 +156,67 @@ __global__ __launch_bounds__(256) void quantize_tiles_kernel(const T* __restrict
     const int64_t row = tr * 32 + r;
     float v[8];
     load8(x, cols, row, col, col_ok && row < rows, v);
+    if constexpr (NORM) {
+      if (col_ok && row < rows) {
+        const float iv = inv[row];
+        float g[8];
+        load8(gamma, 0, 0, col, true, g);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float t = v[j] * iv;   // two roundings, in this order
+          v[j] = t * g[j];
+        }
+      }
+    }
     uint32_t sc;
     const uint32_t w = quantize8(v, G, sc);
     code_tile[r * 8 + c] = w;
     if ((c & 1) == 0) scale_tile[r * 4 + (c >> 1)] = (uint8_t)sc;
+  }
+}
+
+// ------------------------------------------------------------ RMSNorm rows
+// One wavefront per row: ss = sum of the squares (each exact in fp64) in
+// fp64, ms = fp32(ss / K), inv = fp32(1 / fp32(sqrt(fp32(ms + eps))))
+// (correctly rounded square root and division).  With amax != nullptr also
+// the maximum |fp32(fp32(x * inv) * gamma)| of the row (dynamic global scale).
+__global__ __launch_bounds__(256) void rms_rows_kernel(const uint16_t* __restrict__ x,
+                                                       const uint16_t* __restrict__ gamma, float eps, int64_t M,
+                                                       int64_t K, float* __restrict__ inv, float* amax) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;   // uniform over the wavefront
+  const uint16_t* xr = x + row * K;
+  double ss = 0.0;
+  for (int64_t k = lane * 8; k < K; k += 512) {   // K % 16 == 0
+    const uint4_t w = *reinterpret_cast<const uint4_t*>(xr + k);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const double a = bf16_lo(w[j]), b = bf16_hi(w[j]);
+      ss += a * a;
+      ss += b * b;
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, 64);
+  const float ms = (float)(ss / (double)K);
+  const float r = ms + eps;
+  const float iv = 1.0f / sqrtf(r);
+  if (lane == 0) inv[row] = iv;
+  if (amax != nullptr) {
+    float m = 0.0f;
+    for (int64_t k = lane * 8; k < K; k += 512) {
+      const uint4_t w = *reinterpret_cast<const uint4_t*>(xr + k);
+      const uint4_t g = *reinterpret_cast<const uint4_t*>(gamma + k);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float t0 = bf16_lo(w[j]) * iv, t1 = bf16_hi(w[j]) * iv;
+        m = fmaxf(m, fabsf(t0 * bf16_lo(g[j])));
+        m = fmaxf(m, fabsf(t1 * bf16_hi(g[j])));
+      }
+    }
+    m = wave_max(m);
+    if (lane == 0) atomic_max_nonneg(amax, m);
   }
 }
 
@@ -202,6 +261,46 @@ hipError_t launch_quantize_act(const uint16_t* X, int64_t M, int64_t K, const fl
     return launch_quantize(X, M, K, out.G, out, s);
   }
   return launch_quantize(X, M, K, G_static, out, s);
+}
+
+hipError_t launch_rmsnorm_quantize_act(const uint16_t* X, const uint16_t* gamma, float eps, int64_t M, int64_t K,
+                                       const float* G_static, const NvFp4View& out, void* ws, hipStream_t s) {
+  const int64_t tiles_r = round_up(M, 32) / 32, tiles_c = round_up(K, 64) / 64;
+  if (M == 0 || K == 0) {   // nothing to normalize: an all-zero tensor (G = 1 when dynamic)
+    if (G_static == nullptr) {
+      hipLaunchKernelGGL(zero_float_kernel, dim3(1), dim3(1), 0, s, out.G);
+      hipLaunchKernelGGL(finalize_global_scale_kernel, dim3(1), dim3(1), 0, s, out.G);
+      return launch_quantize(X, M, K, out.G, out, s);
+    }
+    return launch_quantize(X, M, K, G_static, out, s);
+  }
+  float* inv = reinterpret_cast<float*>(ws);
+  const bool pooled = inv == nullptr;
+  hipError_t e = hipSuccess;
+  if (pooled) {
+    e = pool_alloc_async(reinterpret_cast<void**>(&inv), (size_t)M * 4, s);
+    if (e != hipSuccess) return e;
+  }
+  const float* Gp = G_static;
+  if (G_static == nullptr) {
+    hipLaunchKernelGGL(zero_float_kernel, dim3(1), dim3(1), 0, s, out.G);
+    hipLaunchKernelGGL(rms_rows_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, s, X, gamma, eps, M, K, inv,
+                       out.G);
+    hipLaunchKernelGGL(finalize_global_scale_kernel, dim3(1), dim3(1), 0, s, out.G);
+    Gp = out.G;
+  } else {
+    hipLaunchKernelGGL(rms_rows_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, s, X, gamma, eps, M, K, inv,
+                       nullptr);
+  }
+  const int64_t blocks = (tiles_r * tiles_c + 3) / 4;
+  hipLaunchKernelGGL((quantize_tiles_kernel<uint16_t, true>), dim3((unsigned)blocks), dim3(256), 0, s, X, M, K, Gp,
+                     out.codes, out.scales, tiles_r, tiles_c, Gp == out.G ? nullptr : out.G, inv, gamma);
+  e = hipGetLastError();
+  if (pooled) {
+    const hipError_t f = hipFreeAsync(inv, s);
+    if (e == hipSuccess) e = f;
+  }
+  return e;
 }
 
 hipError_t launch_pack_nvfp4(const float* W, int64_t N, int64_t K, const float* G_override,

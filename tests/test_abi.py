@@ -160,6 +160,16 @@ def test_invalid_arguments_rejected_on_host():
     assert lib.dq_decode_gemv_nvfp4_workspace_size(4, ctypes.byref(wn), ctypes.byref(ws)) == dq.DQ_OK and ws.value > 0
     assert lib.dq_decode_gemv_nvfp4(fake, 4, ctypes.byref(wn), 0, fake, fake, ws.value - 16,
                                     None) == dq.DQ_ERR_INVALID_ARG
+    # fused RMSNorm quantizer: K % 16, negative / non-finite eps, NULL gamma
+    dn = _nv(4, 64, fake, fake, fake)
+    assert lib.dq_rmsnorm_quantize_act_nvfp4(fake, fake, 1e-6, 4, 24, None, ctypes.byref(_nv(4, 24, fake, fake, fake)),
+                                             None, 0, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_rmsnorm_quantize_act_nvfp4(fake, fake, -1.0, 4, 64, None, ctypes.byref(dn), None, 0, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_rmsnorm_quantize_act_nvfp4(fake, fake, float("nan"), 4, 64, None, ctypes.byref(dn),
+                                             None, 0, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_rmsnorm_quantize_act_nvfp4(fake, None, 1e-6, 4, 64, None, ctypes.byref(dn), None, 0, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_rmsnorm_quantize_act_nvfp4(fake, fake, 1e-6, 4, 64, None, ctypes.byref(dn), fake, 8,
+                                             None) == dq.DQ_ERR_INVALID_ARG
     # autocast: output shape must match W
     assert lib.dq_autocast_lut_to_nvfp4(ctypes.byref(lw), None, ctypes.byref(_nv(16, 64, fake, fake, fake)),
                                         None) == dq.DQ_ERR_INVALID_ARG

@@ -464,3 +464,47 @@ def test_lut_autocast_static_scale():
     q_ref, c_ref, _ = lut.autocast_to_nvfp4(lut.dequantize_per_row(codes_ref, table), G=G)
     q, c, _, _ = L.nvfp4_unpack(host(Wn.codes), host(Wn.scales), 48, 256)
     assert host(Wn.G)[0] == G and np.array_equal(q, q_ref) and np.array_equal(c, c_ref)
+
+
+# ---------------------------------------------------------------- RMSNorm + NVFP4 activation quantization
+from oracle import norm  # noqa: E402
+
+NORM_SHAPES = [(128, 512, 0), (33, 1040, 1), (1, 16, 2), (2048, 4096, 3), (300, 5120, 4)]
+
+
+def _norm_case(M, K, seed):
+    xb = synth.random_bf16(120 + seed, (M, K), outlier_frac=0.005, outlier_factor=30)
+    gb = synth.bf16_bits_from_f32((1.0 + 0.2 * synth.random_f32(121 + seed, (1, K))).astype(np.float32))[0]
+    return xb, gb
+
+
+@pytest.mark.parametrize("M,K,seed", NORM_SHAPES)
+@pytest.mark.parametrize("static", [False, True])
+def test_rmsnorm_quantize_act(M, K, seed, static):
+    """Fused RMSNorm + NVFP4 activation quantization against the oracle's
+    fp32 RMSNorm and a1 quantizer.  Both follow the same fp32 operation
+    order; only the fp64 sum of squares may round differently (tree vs
+    exactly rounded), so a differing code or scale is accepted only at a
+    rounding boundary of the oracle's normalized values, and at most one in
+    10^4."""
+    from test_gpu_epilogue import tolerant_match
+    say("rmsnorm quant", M, K, static)
+    xb, gb = _norm_case(M, K, seed)
+    eps = 1e-5
+    G_s = np.float32(0.0125) if static else None
+    q_ref, c_ref, G_ref, y = norm.quantize_rmsnorm_bf16(xb, gb, eps, G_s)
+    t = dq.dq_rmsnorm_quantize_act_nvfp4(bf16_dev(xb), bf16_dev(gb), eps,
+                                         G_static=dev(np.array([G_s], np.float32)) if static else None)
+    q, c, qfull, cfull = L.nvfp4_unpack(host(t.codes), host(t.scales), M, K)
+    G = host(t.G)[0]
+    assert G == G_ref
+    n_s, n_q = tolerant_match(q, c, y.astype(np.float64), G)
+    say("  differing scales / codes", n_s, n_q)
+    assert n_s + n_q <= max(1, M * K // 10000)
+    assert not qfull[M:].any() and not cfull[M:].any()
+
+
+def test_rmsnorm_quantize_act_empty():
+    t = dq.dq_rmsnorm_quantize_act_nvfp4(torch.empty((0, 64), dtype=torch.int16, device="cuda"),
+                                         torch.ones(64, dtype=torch.bfloat16, device="cuda"))
+    assert t.rows == 0 and host(t.G)[0] == 1.0
