@@ -85,21 +85,22 @@ int num_cus();
 // stream.
 hipError_t pool_alloc_async(void** p, size_t bytes, hipStream_t s);
 
-// Column split of an M x N GEMM between workgroup tiles of bm x bn_full
-// (columns 0 .. split-1) and bm x bn_half (the rest), one workgroup per CU:
-// the split minimises the modelled time, a round of full tiles costing 1 and
-// a round of half-width tiles kHalfRound, ties going to more full tiles.
-// Returns a multiple of bn_full, or N.
+// Column split of an M x N GEMM between workgroup tiles of bm_full x bn_full
+// (columns 0 .. split-1) and smaller tiles of bm_half x bn_half (the rest),
+// `slots` resident workgroups: the split minimises the modelled time, a round
+// of full tiles costing 1 and a round of small tiles half_cost, ties going to
+// more full tiles.  Returns a multiple of bn_full, or N.
 constexpr double kHalfRound = 0.65;
-inline int64_t gemm_column_split(int64_t M, int64_t N, int64_t bm, int64_t bn_full, int64_t bn_half, int64_t cus) {
-  const int64_t tm = (M + bm - 1) / bm;
+inline int64_t gemm_column_split(int64_t M, int64_t N, int64_t bm_full, int64_t bn_full, int64_t bm_half,
+                                 int64_t bn_half, int64_t slots, double half_cost) {
+  const int64_t tm = (M + bm_full - 1) / bm_full, tmh = (M + bm_half - 1) / bm_half;
   const int64_t panels = (N + bn_full - 1) / bn_full;
   int64_t best = panels;
   double best_cost = 1e300;
   for (int64_t p = panels; p >= 0; --p) {
     const int64_t split = p * bn_full < N ? p * bn_full : N;
-    const int64_t full = tm * p, half = tm * ((N - split + bn_half - 1) / bn_half);
-    const double cost = (double)((full + cus - 1) / cus) + kHalfRound * (double)((half + cus - 1) / cus);
+    const int64_t full = tm * p, half = tmh * ((N - split + bn_half - 1) / bn_half);
+    const double cost = (double)((full + slots - 1) / slots) + half_cost * (double)((half + slots - 1) / slots);
     if (cost < best_cost - 1e-9) {
       best_cost = cost;
       best = p;

@@ -35,6 +35,7 @@
 //    output tile: each lane holds 4 consecutive output columns;
 //  * output tiles are handed out in bands of row panels, each XCD taking a
 //    compact sub-block of the tiles in flight (gemm_tile_of).
+#include <algorithm>
 #include <type_traits>
 
 #include "dq_device.hpp"
@@ -45,6 +46,13 @@ namespace dq {
 namespace {
 
 constexpr int kLdsBudget = 150 * 1024;   // of gfx950's 160 KiB
+// modelled cost of a round of 128x128 tiles against one of 256x128 tiles
+// (measured about 0.74 on the 8B up-projection: the smaller tiles dequantize
+// a third more operand elements per MFMA)
+#ifndef DQ_GEMM_SMALL_ROUND
+#define DQ_GEMM_SMALL_ROUND 0.75
+#endif
+constexpr double kSmallRound = DQ_GEMM_SMALL_ROUND;
 
 // Workgroup geometry: WM x WN wavefronts, each owning 32*TM rows x 32*TN
 // columns; one 64-column K step per LDS stage; OCC workgroups per compute
@@ -137,12 +145,20 @@ __device__ inline uint32_t e2m1_code(float v, float S) {
   return fp4_canonical_zero(cvt_pk_fp4<0>(0u, div_by_scale(v, S, rcp), 0.0f)) & 0xFu;
 }
 
+// Workgroup tiles of one geometry: tiles_m x tiles_n tiles over the output
+// columns from n_off on.
+struct Panels {
+  int64_t tiles_m, tiles_n, n_off;
+};
+
+// Workgroup tile blk (0 .. P.tiles_m * P.tiles_n - 1) of geometry Gm.
 template <class Gm, int OUT, bool SW>
-__global__ __launch_bounds__(Gm::threads, Gm::occ) void nvfp4_gemm_kernel(
-    const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales, const float* __restrict__ Ga,
-    const uint8_t* __restrict__ w_codes, const uint8_t* __restrict__ w_scales, const float* __restrict__ Gw,
-    int64_t M, int64_t N, int64_t a_tiles_r, int64_t w_tiles_r, int64_t KT, GemmOut out,
-    int64_t tiles_m, int64_t tiles_n, int64_t n_off) {
+__device__ __forceinline__ void gemm_tile(
+    int64_t blk, const Panels& P, const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
+    const float* __restrict__ Ga, const uint8_t* __restrict__ w_codes, const uint8_t* __restrict__ w_scales,
+    const float* __restrict__ Gw, int64_t M, int64_t N, int64_t a_tiles_r, int64_t w_tiles_r, int64_t KT,
+    const GemmOut& out) {
+  const int64_t n_off = P.n_off;
   constexpr int S = Gm::stages;
   constexpr int TM = Gm::tm, TN = Gm::tn;
   constexpr int L = Gm::loads_per_wave;
@@ -154,7 +170,7 @@ __global__ __launch_bounds__(Gm::threads, Gm::occ) void nvfp4_gemm_kernel(
   // direct loads lives in M0 and must not look divergent to the compiler
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   int64_t bm, bn;
-  gemm_tile_of(blockIdx.x, tiles_m, tiles_n, bm, bn);
+  gemm_tile_of(blk, P.tiles_m, P.tiles_n, bm, bn);
   const int wm = wave % Gm::wm, wn = wave / Gm::wm;
   // this launch covers tiles_n column panels from output column n_off on
   const int64_t a_tr0 = bm * Gm::at, w_tr0 = n_off / 32 + bn * Gm::wt;
@@ -434,16 +450,36 @@ __global__ __launch_bounds__(Gm::threads, Gm::occ) void nvfp4_gemm_kernel(
   }
 }
 
-// Launch geometry Gm over output columns n_off .. n_end-1 (n_off a multiple
-// of 256; n_end a multiple of Gm::bn, or N).
-template <class Gm>
-hipError_t launch_geo(const GemmArgs& a, int64_t n_off, int64_t n_end, hipStream_t s) {
+// One launch, two geometries: workgroups 0 .. big tiles - 1 take the tiles
+// of Gm (columns 0 .. split - 1), the rest those of Gh (columns split ..).
+template <class Gm, class Gh, int OUT, bool SW>
+__global__ __launch_bounds__(Gm::threads, Gm::occ) void nvfp4_gemm_kernel(
+    const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales, const float* __restrict__ Ga,
+    const uint8_t* __restrict__ w_codes, const uint8_t* __restrict__ w_scales, const float* __restrict__ Gw,
+    int64_t M, int64_t N, int64_t a_tiles_r, int64_t w_tiles_r, int64_t KT, GemmOut out, Panels big, Panels small) {
+  static_assert(Gm::threads == Gh::threads && Gm::occ == Gh::occ, "one launch shape");
+  const int64_t nb = big.tiles_m * big.tiles_n;
+  const int64_t b = blockIdx.x;
+  if (b < nb)
+    gemm_tile<Gm, OUT, SW>(b, big, a_codes, a_scales, Ga, w_codes, w_scales, Gw, M, N, a_tiles_r, w_tiles_r, KT, out);
+  else
+    gemm_tile<Gh, OUT, SW>(b - nb, small, a_codes, a_scales, Ga, w_codes, w_scales, Gw, M, N, a_tiles_r, w_tiles_r, KT,
+                           out);
+}
+
+// One launch: output columns 0 .. split-1 in Gm tiles, split .. N-1 in Gh
+// tiles (split a multiple of Gm::bn and of 128, so that an NVFP4 output tile
+// of the SwiGLU half-width result never straddles the two; or N).
+template <class Gm, class Gh>
+hipError_t launch_geo(const GemmArgs& a, int64_t split, hipStream_t s) {
   const int64_t a_tiles_r = round_up(a.M, 32) / 32;
   const int64_t w_tiles_r = round_up(a.N, 32) / 32;
   const int64_t KT = round_up(a.K, 64) / 64;
-  const int64_t tiles_m = (a.M + Gm::bm - 1) / Gm::bm, tiles_n = (n_end - n_off + Gm::bn - 1) / Gm::bn;
-  const size_t lds = (size_t)Gm::stages * Gm::bytes;
-  static_assert(Gm::stages * Gm::bytes <= kLdsBudget, "LDS budget");
+  const Panels big{(a.M + Gm::bm - 1) / Gm::bm, (split + Gm::bn - 1) / Gm::bn, 0};
+  const Panels small{split < a.N ? (a.M + Gh::bm - 1) / Gh::bm : 0, (a.N - split + Gh::bn - 1) / Gh::bn, split};
+  const int64_t blocks = big.tiles_m * big.tiles_n + small.tiles_m * small.tiles_n;
+  const size_t lds = std::max((size_t)Gm::stages * Gm::bytes, (size_t)Gh::stages * Gh::bytes);
+  static_assert(Gm::stages * Gm::bytes <= kLdsBudget && Gh::stages * Gh::bytes <= kLdsBudget, "LDS budget");
   const bool sw = (a.flags & 1) != 0;
   GemmOut o{};
   o.Y = a.Y;
@@ -457,18 +493,17 @@ hipError_t launch_geo(const GemmArgs& a, int64_t n_off, int64_t n_end, hipStream
     o.tiles_c = round_up(o.Nout, 64) / 64;
   }
   typedef void (*kern_t)(const uint8_t*, const uint8_t*, const float*, const uint8_t*, const uint8_t*, const float*,
-                         int64_t, int64_t, int64_t, int64_t, int64_t, GemmOut, int64_t, int64_t, int64_t);
+                         int64_t, int64_t, int64_t, int64_t, int64_t, GemmOut, Panels, Panels);
   static const kern_t kerns[3][2] = {
-      {nvfp4_gemm_kernel<Gm, kOutF32, false>, nvfp4_gemm_kernel<Gm, kOutF32, true>},
-      {nvfp4_gemm_kernel<Gm, kOutBF16, false>, nvfp4_gemm_kernel<Gm, kOutBF16, true>},
-      {nvfp4_gemm_kernel<Gm, kOutNvfp4, false>, nvfp4_gemm_kernel<Gm, kOutNvfp4, true>}};
+      {nvfp4_gemm_kernel<Gm, Gh, kOutF32, false>, nvfp4_gemm_kernel<Gm, Gh, kOutF32, true>},
+      {nvfp4_gemm_kernel<Gm, Gh, kOutBF16, false>, nvfp4_gemm_kernel<Gm, Gh, kOutBF16, true>},
+      {nvfp4_gemm_kernel<Gm, Gh, kOutNvfp4, false>, nvfp4_gemm_kernel<Gm, Gh, kOutNvfp4, true>}};
   const kern_t kern = kerns[a.out_kind][sw ? 1 : 0];
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_m * tiles_n)), dim3(Gm::threads), lds, s, a.A.codes, a.A.scales,
-                     a.A.G, a.W.codes, a.W.scales, a.W.G, a.M, a.N, a_tiles_r, w_tiles_r, KT, o, tiles_m, tiles_n,
-                     n_off);
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(Gm::threads), lds, s, a.A.codes, a.A.scales, a.A.G,
+                     a.W.codes, a.W.scales, a.W.G, a.M, a.N, a_tiles_r, w_tiles_r, KT, o, big, small);
   return hipGetLastError();
 }
 
@@ -484,13 +519,21 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     return hipGetLastError();
   }
   // 256x128 workgroup tiles as 2x2 wavefronts of 128x64, two workgroups per
-  // compute unit (two wavefronts per SIMD): one wavefront's dequantization
+  // compute unit (two wavefronts per SIMD): one workgroup's dequantization
   // and barrier waits overlap the other's MFMAs, and a workgroup's output
-  // stores overlap the other's main loop.  Measured 3-7 % faster than one
-  // workgroup of 128x128 wavefronts per compute unit on the 8B and 27B
-  // shapes.
+  // stores overlap the other's main loop.  A last round that would leave
+  // compute units with one workgroup instead runs its columns as 128x128
+  // tiles (2x2 wavefronts of 64x64), twice as many workgroups of half the
+  // work, in the same launch.
   using Gm = Geo<4, 2, 2, 2, 2>;
-  return launch_geo<Gm>(a, 0, a.N, s);
+  using Gh = Geo<2, 2, 2, 2, 2>;
+  const int64_t slots = (int64_t)num_cus() * Gm::occ;
+#if defined(DQ_GEMM_GEO) && DQ_GEMM_GEO == 1
+  const int64_t split = a.N;
+#else
+  const int64_t split = gemm_column_split(a.M, a.N, Gm::bm, Gm::bn, Gh::bm, Gh::bn, slots, kSmallRound);
+#endif
+  return launch_geo<Gm, Gh>(a, split, s);
 }
 
 }  // namespace dq

@@ -433,7 +433,7 @@ hipError_t launch_mx_gemm(const MxGemmArgs& a, hipStream_t s) {
   // remaining column panels.
   using Full = MxGeo<4, 4, 2, 2>;
   using Half = MxGeo<4, 2, 2, 2>;
-  const int64_t n_split = gemm_column_split(a.M, a.N, Full::bm, Full::bn, Half::bn, num_cus());
+  const int64_t n_split = gemm_column_split(a.M, a.N, Full::bm, Full::bn, Full::bm, Half::bn, num_cus(), kHalfRound);
   hipError_t e = hipSuccess;
   if (n_split > 0) e = launch_mx_geo<Full>(a, 0, n_split, s);
   if (e == hipSuccess && n_split < a.N) e = launch_mx_geo<Half>(a, n_split, a.N, s);

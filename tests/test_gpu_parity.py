@@ -210,6 +210,53 @@ def test_gemm_end_to_end_c1_sampled_rows():
     assert err <= TOL
 
 
+@pytest.mark.parametrize("M,N,K,out", [(2048, 12288, 256, "bf16"), (1024, 20480, 128, "nvfp4"),
+                                       (4096, 5120, 128, "swiglu")])
+def test_gemm_tile_geometries_agree(M, N, K, out):
+    """Shapes whose launch mixes 256x128 tiles (the leading columns) with
+    128x128 tiles (the trailing columns, the last round): each output is
+    accumulated over K in the same order in both, so slices of 32 rows (launched
+    with 128x128 tiles only) equal the full call bit for bit; sampled rows of
+    the full call also match the oracle."""
+    say("geometries", M, N, K, out)
+    xb = synth.random_bf16(90, (M, K), outlier_frac=0.01, outlier_factor=20)
+    w = synth.random_f32(91, (N, K), 0.02)
+    G_x = nvfp4.global_scale(nvfp4.amax(formats.f32_from_bf16_bits(xb)))
+    Gd = dev(np.array([G_x], np.float32))
+    W = dq.dq_pack_nvfp4(dev(w))
+    kw = {}
+    if out == "bf16":
+        kw = dict(out_kind=dq.OUT_BF16)
+    elif out == "nvfp4":
+        kw = dict(out_kind=dq.OUT_NVFP4, G_out_static=dev(np.array([0.02], np.float32)))
+    else:
+        kw = dict(out_kind=dq.OUT_NVFP4, G_out_static=dev(np.array([0.02], np.float32)), epilogue_flags=dq.EPI_SWIGLU)
+    Nout = N // 2 if out == "swiglu" else N
+
+    def run(rows):
+        A = dq.dq_quantize_act_nvfp4(bf16_dev(xb[rows]), G_static=Gd)
+        Y = dq.dq_prefill_gemm(W, A=A, **kw)
+        torch.cuda.synchronize()
+        if out == "bf16":
+            return host(Y.view(torch.int16))
+        q, c, _, _ = L.nvfp4_unpack(host(Y.codes), host(Y.scales), len(rows), Nout)
+        return np.concatenate([q, np.repeat(c, 16, axis=1)], axis=1)
+
+    full = run(np.arange(M))
+    for r0 in (0, M // 2 + 32, M - 32):
+        rows = np.arange(r0, r0 + 32)
+        assert np.array_equal(run(rows), full[rows]), f"rows {r0}..{r0 + 31} differ"
+    if out == "bf16":
+        rows = np.sort(np.random.default_rng(92).choice(M, 8, replace=False))
+        qa, ca, _ = nvfp4.quantize_bf16_activations(xb[rows], G_x)
+        qw, cw, Gw = nvfp4.quantize_dynamic(w)
+        ref = linalg.nvfp4_gemm(qa, ca, G_x, qw, cw, Gw)
+        y = full[rows].view(np.uint16)
+        err = linalg.rel_fro(formats.f64_from_bf16_bits(y), formats.bf16_rne_from_f64(ref))
+        say("  sampled rel_fro", err)
+        assert err <= TOL
+
+
 FUSED_SHAPES = [(128, 512, 512), (300, 520, 1024), (1, 16, 64), (0, 32, 64)]
 
 
