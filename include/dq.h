@@ -261,11 +261,15 @@ dq_status dq_autocast_lut_to_nvfp4(const dq_lut_t* W, const float* G_override, c
  * y[b, n] = sum_k x[b, k] * w_hat[n, k], w_hat = e2m1 * e4m3(scale) * G.
  * x: device bf16 [B, K] row-major, 1 <= B <= 16.  W: NVFP4 weights as packed
  * by dq_pack_nvfp4 (rows = N, cols = K).  out_kind DQ_OUT_F32 / DQ_OUT_BF16:
- * y is device [B, N] row-major.  workspace / workspace_bytes as for
- * dq_decode_gemv (partial sums over K groups; NULL takes stream-ordered
- * memory from the library's pool).  Activations are staged as fp16 after a
- * power-of-two rescale per batch row and K group (the conversion described
- * for dq_decode_gemv); weight products are exact, sums fp32. */
+ * y is device [B, N] row-major; x 16-byte aligned.  Small batches (B <= 8,
+ * at most 2 row tiles of 32 per compute unit, B * K within the staging
+ * limit) run in one launch that splits K inside each workgroup and needs no
+ * workspace (dq_decode_gemv_nvfp4_workspace_size reports 0); otherwise
+ * workspace / workspace_bytes are as for dq_decode_gemv (partial sums over K
+ * groups; NULL takes stream-ordered memory from the library's pool).
+ * Activations are staged as fp16 after a power-of-two rescale per batch row
+ * and K slice (the conversion described for dq_decode_gemv); weight products
+ * are exact, sums fp32. */
 dq_status dq_decode_gemv_nvfp4_workspace_size(int64_t B, const dq_nvfp4_t* W, size_t* bytes);
 dq_status dq_decode_gemv_nvfp4(const uint16_t* x, int64_t B, const dq_nvfp4_t* W, int out_kind, void* y,
                                void* workspace, size_t workspace_bytes, void* stream);

@@ -61,12 +61,13 @@ __device__ inline int nv_stage_exponent(uint32_t mb) {
 }
 
 constexpr int kNvWaves = 4;
+constexpr int kCyc = 4;   // K steps per cycle of code loads
 
-// Workgroup (K group kg, tile group tg) of 4 wavefronts (two workgroups per
+// Workgroup (K group kg, tile group tg) of 4 wavefronts (four workgroups per
 // compute unit).  The K group's
 // slice of x (all B rows, KCR = 8 KC8 steps of 64 columns) is staged once in
 // LDS as fp16; wavefront w then owns tiles (tg * 8 + w) * TPW + i, i < TPW,
-// each over the whole K group, in cycles of 8 steps: the code and scale loads
+// each over the whole K group, in cycles of kCyc steps: the code and scale loads
 // of cycle q+1 are issued before cycle q is consumed (a fixed count, so the
 // compiler's wait for them is exact); tiles and steps past the end read zeros
 // through range-checked buffer loads, without touching memory.
@@ -94,20 +95,21 @@ __global__ __launch_bounds__(256) void nvfp4_gemv_kernel(const uint16_t* __restr
   const int s_off = 4 * r + 2 * h;                    // E4M3 scales of blocks 2h, 2h+1 of row r
   const int tile0 = (tg * kNvWaves + wave) * TPW;
 
-  // loads of cycle q (tile tile0 + q / KC8, steps 8 (q % KC8) .. +7) into
-  // buffer BUF (a compile-time index: the buffers must stay in registers)
+  // loads of cycle q (tile tile0 + q / CPT, steps kCyc (q % CPT) .. +kCyc-1)
+  // into one of two named buffers (they must stay in registers)
   struct Cycle {
-    uint4_t c[8];
-    uint32_t s[8];
+    uint4_t c[kCyc];
+    uint32_t s[kCyc];
   };
+  constexpr int CPT = KCR / kCyc;                     // cycles per tile
   Cycle cb0, cb1;
   auto issue = [&](int q, Cycle& cb) {
-    const int t = tile0 + q / KC8, st0 = 8 * (q % KC8);
+    const int t = tile0 + q / CPT, st0 = kCyc * (q % CPT);
     const bool ok = t < T;
     const v4i_t rc = nv_resource(codes + ((int64_t)(ok ? t : 0) * KT + kt0) * 1024, ok ? (uint32_t)valid * 1024u : 0u);
     const v4i_t rs = nv_resource(scales + ((int64_t)(ok ? t : 0) * KT + kt0) * 128, ok ? (uint32_t)valid * 128u : 0u);
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < kCyc; ++u) {
       const v4i_t v = nv_buffer_load_b128(rc, c_off, (st0 + u) * 1024, 0);
       cb.c[u] = uint4_t{(uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]};
       cb.s[u] = (uint16_t)nv_buffer_load_b16(rs, s_off, (st0 + u) * 128, 0);
@@ -155,16 +157,17 @@ __global__ __launch_bounds__(256) void nvfp4_gemv_kernel(const uint16_t* __restr
   const int b_l = r < B ? r : B;
   const _Float16* xl = xs + b_l * kRow + 32 * h;
   const float us = s_unscale[r < B ? r : 0];
-  // four accumulators (one per sub-step) keep consecutive MFMAs independent;
-  // the sched_barrier after every step keeps the compiler from hoisting the
-  // LDS reads and dequantization of a whole cycle (and their registers)
-  float16_t acc[4];
+  // two accumulators (even and odd sub-steps) keep consecutive MFMAs
+  // independent; the sched_barrier after every step keeps the compiler from
+  // hoisting the LDS reads and dequantization of a whole cycle (and their
+  // registers)
+  float16_t acc[2];
 #pragma unroll
-  for (int s = 0; s < 4; ++s) acc[s] = float16_t{};
+  for (int s = 0; s < 2; ++s) acc[s] = float16_t{};
   auto consume = [&](int q, const Cycle& cb) {
-    const int st0 = 8 * (q % KC8);
+    const int st0 = kCyc * (q % CPT);
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < kCyc; ++u) {
       const half2_t sp = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(cb.s[u], 1.0f, false);
       const half2_t s_lo = half2_t{sp[0], sp[0]}, s_hi = half2_t{sp[1], sp[1]};
       half8_t xb[4];
@@ -172,18 +175,18 @@ __global__ __launch_bounds__(256) void nvfp4_gemv_kernel(const uint16_t* __restr
       for (int s = 0; s < 4; ++s) xb[s] = *reinterpret_cast<const half8_t*>(xl + (st0 + u) * 64 + 8 * s);
 #pragma unroll
       for (int s = 0; s < 4; ++s)
-        acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_f16(nv_dequant8(cb.c[u][s], s < 2 ? s_lo : s_hi), xb[s], acc[s],
-                                                        0, 0, 0);
+        acc[s & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(nv_dequant8(cb.c[u][s], s < 2 ? s_lo : s_hi), xb[s],
+                                                            acc[s & 1], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (q % KC8 == KC8 - 1) {   // end of a tile: its sum over the K group
-      const int t = tile0 + q / KC8;
+    if (q % CPT == CPT - 1) {   // end of a tile: its sum over the K group
+      const int t = tile0 + q / CPT;
       if (t < T && r < B) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int64_t row = (int64_t)t * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
           if (row >= N) continue;
-          const float v = ((acc[0][i] + acc[1][i]) + (acc[2][i] + acc[3][i])) * us;
+          const float v = (acc[0][i] + acc[1][i]) * us;
           if (partials != nullptr) {
             partials[((int64_t)kg * B + r) * N + row] = v;
           } else if (out_kind == 0) {
@@ -194,10 +197,10 @@ __global__ __launch_bounds__(256) void nvfp4_gemv_kernel(const uint16_t* __restr
         }
       }
 #pragma unroll
-      for (int s = 0; s < 4; ++s) acc[s] = float16_t{};
+      for (int s = 0; s < 2; ++s) acc[s] = float16_t{};
     }
   };
-  const int cycles = TPW * KC8;
+  const int cycles = TPW * CPT;
   int q = 0;
   for (; q + 2 <= cycles; q += 2) {
     issue(q + 1, cb1);
@@ -206,6 +209,162 @@ __global__ __launch_bounds__(256) void nvfp4_gemv_kernel(const uint16_t* __restr
     consume(q + 1, cb1);
   }
   if (q < cycles) consume(q, cb0);
+}
+
+// One-launch kernel for small batches (B <= 8 with the staged slices within
+// 48 KiB of LDS) and at most two resident workgroups per compute unit's worth
+// of row tiles.  A workgroup of kKsWaves wavefronts takes one row tile;
+// wavefront w takes K steps [w SPW, (w + 1) SPW).  It copies its own slice of
+// x straight into LDS (issued before its code loads, so the copy is not
+// queued behind them), then per batch row takes the slice maximum, a
+// power-of-two scale and converts in place (no barrier: nothing is shared),
+// streams its codes in cycles of kCyc steps, and parks its unscaled partial
+// sums in LDS.  After the one barrier, the kKsWaves partials of each (batch
+// row, tile row) are added in wavefront order and stored (deterministic).
+constexpr int kKsWaves = 8;
+
+__device__ inline float nv_wave_max(float m) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  return m;
+}
+
+__global__ __launch_bounds__(64 * kKsWaves) void nvfp4_gemv_ks_kernel(
+    const uint16_t* __restrict__ x, int B, int64_t K, const uint8_t* __restrict__ codes,
+    const uint8_t* __restrict__ scales, const float* __restrict__ Gp, int64_t N, int KT, int SPW, int xslots,
+    int out_kind, void* __restrict__ y) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int t = blockIdx.x;
+  const int row_len = SPW * 64;                       // staged fp16 per batch row
+  const int pieces = B * SPW * 8;                     // 8-element pieces of the slice
+  // LDS: per wavefront xslots * 64 pieces of 16 bytes | partials [kKsWaves][B][32]
+  uint8_t* xw_raw = smem + (size_t)wave * xslots * 1024;
+  _Float16* xw = reinterpret_cast<_Float16*>(xw_raw);
+  float* part = reinterpret_cast<float*>(smem + (size_t)kKsWaves * xslots * 1024);
+  const int kt0 = wave * SPW;
+  const int nst = max(0, min(SPW, KT - kt0));         // valid steps of this wavefront
+  const int64_t k0 = (int64_t)kt0 * 64;
+
+  // ---- 1. the slice of x, raw, straight into LDS: piece p (batch row
+  // p / (8 SPW), columns 8 (p % (8 SPW)) ..) lands at byte 16 p; addresses
+  // past K are clamped in bounds and the pieces zeroed at conversion
+  for (int j = 0; j < xslots; ++j) {
+    const int p = min(j * 64 + lane, pieces - 1);
+    const int b = p / (SPW * 8), e = p - b * (SPW * 8);
+    const int64_t k = min(k0 + 8 * e, K - 8);
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(x + (int64_t)b * K + k),
+                                     reinterpret_cast<void*>(xw_raw + j * 1024), 16, 0, 0);
+  }
+
+  // ---- 2. the first two cycles of code loads
+  const int r = lane & 31, h = lane >> 5;
+  const int c_off = 16 * (2 * r + h);
+  const int s_off = 4 * r + 2 * h;
+  const v4i_t rc = nv_resource(codes + ((int64_t)t * KT + kt0) * 1024, (uint32_t)nst * 1024u);
+  const v4i_t rs = nv_resource(scales + ((int64_t)t * KT + kt0) * 128, (uint32_t)nst * 128u);
+  struct Cycle {
+    uint4_t c[kCyc];
+    uint32_t s[kCyc];
+  };
+  Cycle cb0, cb1;
+  auto issue = [&](int q, Cycle& cb) {
+#pragma unroll
+    for (int u = 0; u < kCyc; ++u) {
+      const v4i_t v = nv_buffer_load_b128(rc, c_off, (kCyc * q + u) * 1024, 0);
+      cb.c[u] = uint4_t{(uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]};
+      cb.s[u] = (uint16_t)nv_buffer_load_b16(rs, s_off, (kCyc * q + u) * 128, 0);
+    }
+  };
+  __builtin_amdgcn_sched_barrier(0);
+  issue(0, cb0);
+  issue(1, cb1);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- 3. once the copy has landed (vmcnt: the 4 kCyc code and scale loads
+  // may still be in flight), per batch row: maximum, scale, conversion
+  {
+    constexpr int kv = 4 * kCyc;
+    __builtin_amdgcn_s_waitcnt((kv & 0xF) | ((kv >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  const float G = *Gp;
+  float us = 0.0f;
+  for (int b = 0; b < B; ++b) {
+    uint4_t* rowp = reinterpret_cast<uint4_t*>(xw + (size_t)b * row_len);
+    float m = 0.0f;
+    for (int e = lane; e < SPW * 8; e += 64) {
+      const uint4_t v = rowp[e];
+#pragma unroll
+      for (int w4 = 0; w4 < 4; ++w4) m = fmaxf(m, fmaxf(fabsf(bf16_lo(v[w4])), fabsf(bf16_hi(v[w4]))));
+    }
+    const int ex = nv_stage_exponent(__float_as_uint(nv_wave_max(m)));
+    const float sc = __builtin_ldexpf(1.0f, ex);
+    if (r == b) us = __builtin_ldexpf(1.0f, -ex) * G;
+    for (int e = lane; e < SPW * 8; e += 64) {
+      const uint4_t v = rowp[e];
+      uint4_t o{0u, 0u, 0u, 0u};
+      if (k0 + 8 * e < K) {
+#pragma unroll
+        for (int w4 = 0; w4 < 4; ++w4)   // the scaled values are exact in fp16
+          o[w4] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(bf16_lo(v[w4]) * sc, bf16_hi(v[w4]) * sc));
+      }
+      rowp[e] = o;
+    }
+  }
+
+  // ---- 4. cycles: lane l's x operand is batch row l%32 (row 0 for l%32 >=
+  // B: those MFMA output columns are never stored)
+  const _Float16* xl = xw + (size_t)(r < B ? r : 0) * row_len + 32 * h;
+  float16_t acc[2] = {float16_t{}, float16_t{}};
+  auto consume = [&](int q, const Cycle& cb) {
+#pragma unroll
+    for (int u = 0; u < kCyc; ++u) {
+      const int st = min(kCyc * q + u, SPW - 1);   // past SPW: zero codes, any in-range x
+      const half2_t sp = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(cb.s[u], 1.0f, false);
+      const half2_t s_lo = half2_t{sp[0], sp[0]}, s_hi = half2_t{sp[1], sp[1]};
+      half8_t xb[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) xb[s] = *reinterpret_cast<const half8_t*>(xl + st * 64 + 8 * s);
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        acc[s & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(nv_dequant8(cb.c[u][s], s < 2 ? s_lo : s_hi), xb[s],
+                                                            acc[s & 1], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  const int cycles = (SPW + kCyc - 1) / kCyc;
+  int q = 0;
+  for (; q + 2 <= cycles; q += 2) {
+    consume(q, cb0);
+    issue(q + 2, cb0);   // past the wavefront's steps: zeros without memory traffic
+    consume(q + 1, cb1);
+    issue(q + 3, cb1);
+  }
+  if (q < cycles) consume(q, cb0);
+  // the last cycle's redundant loads (zero reads) drain before the wavefront ends
+  __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));
+
+  // ---- 5. partials, one barrier, fixed-order sum over the wavefronts
+  if (r < B) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      part[(wave * B + r) * 32 + 8 * (i >> 2) + 4 * h + (i & 3)] = (acc[0][i] + acc[1][i]) * us;
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < B * 32) {
+    const int b = threadIdx.x >> 5, rr = threadIdx.x & 31;
+    float v = part[b * 32 + rr];
+    for (int w = 1; w < kKsWaves; ++w) v += part[(w * B + b) * 32 + rr];
+    const int64_t row = (int64_t)t * 32 + rr;
+    if (row < N) {
+      if (out_kind == 0)
+        reinterpret_cast<float*>(y)[(int64_t)b * N + row] = v;
+      else
+        reinterpret_cast<uint16_t*>(y)[(int64_t)b * N + row] = (uint16_t)f32_to_bf16_rne(v);
+    }
+  }
 }
 
 // y[b, n] = sum over K groups, in order, of partials[g, b, n]
@@ -253,10 +412,32 @@ NvGemvPlan nv_plan(int64_t B, int64_t N, int64_t K) {
   return p;
 }
 
+// The one-launch kernel: a workgroup per row tile when the tiles fit two
+// resident workgroups per compute unit and the staged slices fit in LDS.
+struct KsPlan {
+  bool ok;
+  int T, KT, SPW, xslots;
+  size_t lds;
+};
+
+KsPlan ks_plan(int64_t B, int64_t N, int64_t K) {
+  KsPlan p{};
+  const int64_t T = (N + 31) / 32, KT = (K + 63) / 64;
+  const int64_t SPW = (KT + kKsWaves - 1) / kKsWaves;
+  const int64_t xslots = (B * SPW * 8 + 63) / 64;
+  p.lds = (size_t)kKsWaves * (size_t)xslots * 1024 + (size_t)kKsWaves * (size_t)B * 32 * 4;
+  p.ok = B >= 1 && B <= 8 && T <= 2 * (int64_t)num_cus() && p.lds <= 48 * 1024;
+  p.T = (int)T;
+  p.KT = (int)KT;
+  p.SPW = (int)SPW;
+  p.xslots = (int)xslots;
+  return p;
+}
+
 }  // namespace
 
 size_t gemv_nvfp4_workspace_bytes(int64_t B, int64_t N, int64_t K) {
-  if (B < 1 || N == 0 || K == 0) return 0;
+  if (B < 1 || N == 0 || K == 0 || ks_plan(B, N, K).ok) return 0;
   return nv_plan(B, N, K).partial_bytes;
 }
 
@@ -268,6 +449,12 @@ hipError_t launch_gemv_nvfp4(const uint16_t* x, int64_t B, const NvFp4View& w, i
     const int64_t words = (B * N * (out_kind == 0 ? 4 : 2) + 3) / 4;
     hipLaunchKernelGGL(nv_zero_kernel, dim3((unsigned)std::min<int64_t>(1024, (words + 255) / 256)), dim3(256), 0, s,
                        reinterpret_cast<uint32_t*>(y), words);
+    return hipGetLastError();
+  }
+  const KsPlan ks = ks_plan(B, N, K);
+  if (ks.ok) {
+    hipLaunchKernelGGL(nvfp4_gemv_ks_kernel, dim3((unsigned)ks.T), dim3(64 * kKsWaves), ks.lds, s, x, (int)B, K,
+                       w.codes, w.scales, w.G, N, ks.KT, ks.SPW, ks.xslots, out_kind, y);
     return hipGetLastError();
   }
   const NvGemvPlan p = nv_plan(B, N, K);

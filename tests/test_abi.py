@@ -157,8 +157,10 @@ def test_invalid_arguments_rejected_on_host():
     assert lib.dq_decode_gemv_nvfp4(fake, 1, ctypes.byref(_nv(16, 24, fake, fake, fake)), 0, fake, None, 0,
                                     None) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_decode_gemv_nvfp4(fake, 1, None, 0, fake, None, 0, None) == dq.DQ_ERR_INVALID_ARG
-    assert lib.dq_decode_gemv_nvfp4_workspace_size(4, ctypes.byref(wn), ctypes.byref(ws)) == dq.DQ_OK and ws.value > 0
-    assert lib.dq_decode_gemv_nvfp4(fake, 4, ctypes.byref(wn), 0, fake, fake, ws.value - 16,
+    # batch 1 runs in one launch without a workspace; batch 16 splits K
+    assert lib.dq_decode_gemv_nvfp4_workspace_size(1, ctypes.byref(wn), ctypes.byref(ws)) == dq.DQ_OK and ws.value == 0
+    assert lib.dq_decode_gemv_nvfp4_workspace_size(16, ctypes.byref(wn), ctypes.byref(ws)) == dq.DQ_OK and ws.value > 0
+    assert lib.dq_decode_gemv_nvfp4(fake, 16, ctypes.byref(wn), 0, fake, fake, ws.value - 16,
                                     None) == dq.DQ_ERR_INVALID_ARG
     # fused RMSNorm quantizer: K % 16, negative / non-finite eps, NULL gamma
     dn = _nv(4, 64, fake, fake, fake)

@@ -425,8 +425,11 @@ def test_gemv_workspace_and_pool_paths_agree():
 
 
 # ---------------------------------------------------------------- NVFP4A16 decode GEMV
+# one-launch kernel: batch <= 8 with the activation slices in LDS and at most
+# 2 x 256 row tiles; the K-group kernel otherwise ((5120, 5120, 16),
+# (64, 4096, 8), (17408, 2048, 1), (16416, 64, 1))
 NV_GEMV_CASES = [(512, 512, 1), (100, 96, 3), (33, 1040, 2), (7168, 5120, 1), (5120, 17408, 1), (5120, 5120, 16),
-                 (12288, 4096, 4), (64, 4096, 8)]
+                 (12288, 4096, 4), (64, 4096, 8), (17408, 2048, 1), (16416, 64, 1), (16384, 208, 8), (40, 16, 1)]
 
 
 @pytest.mark.parametrize("N,K,B", NV_GEMV_CASES)
@@ -451,12 +454,14 @@ def test_nvfp4a16_gemv(N, K, B):
 
 
 def test_nvfp4a16_gemv_empty_and_pool():
-    """K = 0 gives zeros; a NULL workspace (library pool) gives the same
-    result as a caller workspace."""
+    """K = 0 gives zeros; a small batch runs in one launch without a
+    workspace; with K split over workgroups (batch 12) a NULL workspace
+    (library pool) gives the same result as a caller workspace."""
     W0 = dq.NvFp4Tensor.empty(40, 0)
     y0 = dq.dq_decode_gemv_nvfp4(torch.zeros((2, 0), dtype=torch.int16, device="cuda"), W0)
     assert tuple(y0.shape) == (2, 40) and not host(y0).any()
-    N, K, B = 5120, 5120, 2
+    assert dq.dq_decode_gemv_nvfp4_workspace_size(2, dq.NvFp4Tensor.empty(5120, 5120)) == 0
+    N, K, B = 5120, 5120, 12
     w = _lut_weight(N, K, 92)
     Wq = dq.dq_pack_nvfp4(dev(w))
     xb = synth.random_bf16(93, (B, K), outlier_frac=0.005, outlier_factor=30)
