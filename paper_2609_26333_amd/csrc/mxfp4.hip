@@ -174,11 +174,20 @@ __device__ inline void mx_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Workgroup tiles of one geometry: tiles_m x tiles_n tiles over the output
+// columns from n_off on.
+struct MxPanels {
+  int64_t tiles_m, tiles_n, n_off;
+};
+
+// Workgroup tile blk (0 .. P.tiles_m * P.tiles_n - 1) of geometry Gm.
 template <class Gm, int OUT>
-__global__ __launch_bounds__(Gm::threads, 1) void mxfp4_gemm_kernel(
-    const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales, const uint8_t* __restrict__ w_codes,
-    const uint8_t* __restrict__ w_scales, int64_t M, int64_t N, int64_t a_tiles_r, int64_t w_tiles_r, int64_t KT,
-    void* __restrict__ Y, int64_t tiles_m, int64_t tiles_n, int64_t n_off) {
+__device__ __forceinline__ void mx_gemm_tile(int64_t blk, const MxPanels& P, const uint8_t* __restrict__ a_codes,
+                                             const uint8_t* __restrict__ a_scales,
+                                             const uint8_t* __restrict__ w_codes,
+                                             const uint8_t* __restrict__ w_scales, int64_t M, int64_t N,
+                                             int64_t a_tiles_r, int64_t w_tiles_r, int64_t KT, void* __restrict__ Y) {
+  const int64_t tiles_m = P.tiles_m, tiles_n = P.tiles_n, n_off = P.n_off;
   constexpr int S = Gm::stages;
   constexpr int TM = Gm::tm, TN = Gm::tn;
   constexpr int L = Gm::loads_per_wave;
@@ -187,7 +196,7 @@ __global__ __launch_bounds__(Gm::threads, 1) void mxfp4_gemm_kernel(
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   int64_t bm, bn;
-  gemm_tile_of(blockIdx.x, tiles_m, tiles_n, bm, bn);
+  gemm_tile_of(blk, tiles_m, tiles_n, bm, bn);
   const int wm = wave % Gm::wm, wn = wave / Gm::wm;
   const int64_t a_tr0 = bm * Gm::at, w_tr0 = n_off / 32 + bn * Gm::wt;
   const int64_t m0 = bm * Gm::bm + wm * 32 * TM;
@@ -390,21 +399,41 @@ __global__ __launch_bounds__(Gm::threads, 1) void mxfp4_gemm_kernel(
   }
 }
 
-template <class Gm>
-hipError_t launch_mx_geo(const MxGemmArgs& a, int64_t n_off, int64_t n_end, hipStream_t s) {
+// One launch, two geometries: workgroups 0 .. full tiles - 1 take the tiles
+// of Gf (columns 0 .. split - 1), the rest those of Gh (columns split ..).
+template <class Gf, class Gh, int OUT>
+__global__ __launch_bounds__(Gf::threads, 1) void mxfp4_gemm_kernel(
+    const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales, const uint8_t* __restrict__ w_codes,
+    const uint8_t* __restrict__ w_scales, int64_t M, int64_t N, int64_t a_tiles_r, int64_t w_tiles_r, int64_t KT,
+    void* __restrict__ Y, MxPanels full, MxPanels half) {
+  static_assert(Gf::threads == Gh::threads, "one launch shape");
+  const int64_t nf = full.tiles_m * full.tiles_n;
+  const int64_t b = blockIdx.x;
+  if (b < nf)
+    mx_gemm_tile<Gf, OUT>(b, full, a_codes, a_scales, w_codes, w_scales, M, N, a_tiles_r, w_tiles_r, KT, Y);
+  else
+    mx_gemm_tile<Gh, OUT>(b - nf, half, a_codes, a_scales, w_codes, w_scales, M, N, a_tiles_r, w_tiles_r, KT, Y);
+}
+
+// Output columns 0 .. split-1 in Gf tiles, split .. N-1 in Gh tiles (split a
+// multiple of Gf::bn, or N), one launch.
+template <class Gf, class Gh>
+hipError_t launch_mx_geo(const MxGemmArgs& a, int64_t split, hipStream_t s) {
   const int64_t a_tiles_r = round_up(a.M, 32) / 32;
   const int64_t w_tiles_r = round_up(a.N, 32) / 32;
   const int64_t KT = round_up(a.K, 64) / 64;
-  const int64_t tiles_m = (a.M + Gm::bm - 1) / Gm::bm, tiles_n = (n_end - n_off + Gm::bn - 1) / Gm::bn;
-  const size_t lds = (size_t)Gm::stages * Gm::bytes;
+  const MxPanels full{(a.M + Gf::bm - 1) / Gf::bm, (split + Gf::bn - 1) / Gf::bn, 0};
+  const MxPanels half{split < a.N ? (a.M + Gh::bm - 1) / Gh::bm : 0, (a.N - split + Gh::bn - 1) / Gh::bn, split};
+  const int64_t blocks = full.tiles_m * full.tiles_n + half.tiles_m * half.tiles_n;
+  const size_t lds = std::max((size_t)Gf::stages * Gf::bytes, (size_t)Gh::stages * Gh::bytes);
   typedef void (*kern_t)(const uint8_t*, const uint8_t*, const uint8_t*, const uint8_t*, int64_t, int64_t, int64_t,
-                         int64_t, int64_t, void*, int64_t, int64_t, int64_t);
-  const kern_t kern = a.out_kind == 0 ? mxfp4_gemm_kernel<Gm, 0> : mxfp4_gemm_kernel<Gm, 1>;
+                         int64_t, int64_t, void*, MxPanels, MxPanels);
+  const kern_t kern = a.out_kind == 0 ? mxfp4_gemm_kernel<Gf, Gh, 0> : mxfp4_gemm_kernel<Gf, Gh, 1>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_m * tiles_n)), dim3(Gm::threads), lds, s, a.A.codes, a.A.scales,
-                     a.W.codes, a.W.scales, a.M, a.N, a_tiles_r, w_tiles_r, KT, a.Y, tiles_m, tiles_n, n_off);
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(Gf::threads), lds, s, a.A.codes, a.A.scales, a.W.codes,
+                     a.W.scales, a.M, a.N, a_tiles_r, w_tiles_r, KT, a.Y, full, half);
   return hipGetLastError();
 }
 
@@ -429,15 +458,12 @@ hipError_t launch_mx_gemm(const MxGemmArgs& a, hipStream_t s) {
   if (a.M == 0 || a.N == 0) return hipSuccess;
   // 256x256 workgroup tiles (four wavefronts of 128x128, one per SIMD); one
   // workgroup fills a compute unit, so a last round that would leave compute
-  // units idle runs instead as a second launch of 256x128 tiles over the
-  // remaining column panels.
+  // units idle runs instead as 256x128 tiles over the remaining column
+  // panels, in the same launch.
   using Full = MxGeo<4, 4, 2, 2>;
   using Half = MxGeo<4, 2, 2, 2>;
   const int64_t n_split = gemm_column_split(a.M, a.N, Full::bm, Full::bn, Full::bm, Half::bn, num_cus(), kHalfRound);
-  hipError_t e = hipSuccess;
-  if (n_split > 0) e = launch_mx_geo<Full>(a, 0, n_split, s);
-  if (e == hipSuccess && n_split < a.N) e = launch_mx_geo<Half>(a, n_split, a.N, s);
-  return e;
+  return launch_mx_geo<Full, Half>(a, n_split, s);
 }
 
 }  // namespace dq
