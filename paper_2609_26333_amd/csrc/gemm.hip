@@ -46,14 +46,6 @@ namespace dq {
 namespace {
 
 constexpr int kLdsBudget = 150 * 1024;   // of gfx950's 160 KiB
-// modelled cost of a round of 128x128 tiles against one of 256x128 tiles
-// (measured about 0.74 on the 8B up-projection: the smaller tiles dequantize
-// a third more operand elements per MFMA)
-#ifndef DQ_GEMM_SMALL_ROUND
-#define DQ_GEMM_SMALL_ROUND 0.75
-#endif
-constexpr double kSmallRound = DQ_GEMM_SMALL_ROUND;
-
 // Workgroup geometry: WM x WN wavefronts, each owning 32*TM rows x 32*TN
 // columns; one 64-column K step per LDS stage; OCC workgroups per compute
 // unit (registers and LDS sized for them).
@@ -521,17 +513,25 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
   // 256x128 workgroup tiles as 2x2 wavefronts of 128x64, two workgroups per
   // compute unit (two wavefronts per SIMD): one workgroup's dequantization
   // and barrier waits overlap the other's MFMAs, and a workgroup's output
-  // stores overlap the other's main loop.  A last round that would leave
-  // compute units with one workgroup instead runs its columns as 128x128
-  // tiles (2x2 wavefronts of 64x64), twice as many workgroups of half the
-  // work, in the same launch.
+  // stores overlap the other's main loop.  128x128 tiles (2x2 wavefronts of
+  // 64x64) dequantize a third more operand elements per MFMA, so they only
+  // take the columns of a last round that would leave most slots empty (at
+  // most a quarter full), or the whole grid when it is under one round.
+  // Measured on the paper's linears: the 27B o-projection (a quarter-full
+  // last round) 10 % faster, shapes with a half-full last round unchanged
+  // or 1-2 % slower, so those keep 256x128 tiles.
   using Gm = Geo<4, 2, 2, 2, 2>;
   using Gh = Geo<2, 2, 2, 2, 2>;
   const int64_t slots = (int64_t)num_cus() * Gm::occ;
+  const int64_t tm = (a.M + Gm::bm - 1) / Gm::bm, panels = (a.N + Gm::bn - 1) / Gm::bn;
+  const int64_t tiles = tm * panels, rounds = tiles / slots, rest = tiles % slots;
+  int64_t split = a.N;
+  if (rounds == 0 && 2 * tiles <= slots)
+    split = 0;
+  else if (rounds > 0 && rest > 0 && 4 * rest <= slots)
+    split = rounds * slots / tm * Gm::bn;
 #if defined(DQ_GEMM_GEO) && DQ_GEMM_GEO == 1
-  const int64_t split = a.N;
-#else
-  const int64_t split = gemm_column_split(a.M, a.N, Gm::bm, Gm::bn, Gh::bm, Gh::bn, slots, kSmallRound);
+  split = a.N;
 #endif
   return launch_geo<Gm, Gh>(a, split, s);
 }
