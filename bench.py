@@ -222,7 +222,7 @@ def nvfp4a16_decode(dq, torch, np, Wq, xd_dev, Bs, N, K, s, decode_bytes, reps):
         out[f"b{b}"] = {"us": t * 1e6, "GB/s": alg / t / 1e9, "frac_hbm": alg / t / 1e9 / PEAK_HBM_GBS,
                         "bytes": alg}
     out["weight_copies"] = n_w
-    out["note"] = "NVFP4 weights (4.5 bits), bf16 x, fp16 MFMA; back-to-back calls incl. the K-group reduction pass"
+    out["note"] = "NVFP4 weights (4.5 bits), bf16 x, fp16 MFMA; back-to-back calls; one launch per call at these batches (K split inside each workgroup)"
     return out
 
 
