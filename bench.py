@@ -278,8 +278,8 @@ def decode_sweep(dq, synth, torch, np, n_blocks, steps):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              f"(the sharded design is described in DESIGN.md)", file=sys.stderr)
+        print(f"bench.py: the kernels run on one GPU (one GPU's share of a sharded layer); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
         sys.exit(2)
     if args.calibrate_copy:
         calibrate_copy()
