@@ -41,7 +41,7 @@ extern "C" {
 typedef int32_t dq_status;
 #define DQ_OK 0
 #define DQ_ERR_INVALID_ARG (-1) /* null/misaligned pointer, bad size or enum */
-#define DQ_ERR_UNSUPPORTED (-2) /* valid request this build does not implement */
+#define DQ_ERR_UNSUPPORTED (-2) /* valid request the library does not implement */
 #define DQ_ERR_HIP (-3)         /* a HIP launch failed; see dq_last_error() */
 
 /* Output element kinds. */
