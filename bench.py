@@ -448,7 +448,7 @@ def main():
                     "linear_TFLOP/s_incl_quant": prefill_tflops},
         "decode": decode,
         "pack_ms": {"nvfp4": t_pack_nvfp4, "lut3_per_row": t_pack_lut, "lut3_to_nvfp4_autocast": t_autocast},
-        "roofline": {"bound": "mfma", "kernel": "nvfp4_gemm_kernel (the launches of one dq_prefill_gemm call)",
+        "roofline": {"bound": "mfma", "kernel": "nvfp4_gemm_kernel (one launch per dq_prefill_gemm call)",
                      "achieved": gemm_tflops,
                      "peak": PEAK_FP16_TFLOPS, "unit": "TFLOP/s", "frac": gemm_tflops / PEAK_FP16_TFLOPS,
                      "traffic": traffic,
