@@ -1066,8 +1066,13 @@ inline int persist_wgs_per_cu(int vgprs, int waves, int64_t lds) {
   return std::max(1, std::min(by_vgpr, by_lds));
 }
 
+// Wavefront tasks per compute unit for the batched kernel.  Fewer tasks mean
+// fewer K groups: less partial-sum traffic and less activation staging per
+// weight byte.  Measured over the 27B and 8B decode linears at batch 2-16:
+// 12 is 0-13 % faster than 24 (all but the 27B down-projection at batch 16,
+// 7 % slower), 16 / 32 / 48 in between or slower.
 #ifndef DQ_GEMV_TASKS_PER_CU
-#define DQ_GEMV_TASKS_PER_CU 24
+#define DQ_GEMV_TASKS_PER_CU 12
 #endif
 
 // Plan of the batch B >= 2 split-K kernel (see lut_gemv_split_kernel).
