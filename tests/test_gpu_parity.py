@@ -425,11 +425,12 @@ def test_gemv_workspace_and_pool_paths_agree():
 
 
 # ---------------------------------------------------------------- NVFP4A16 decode GEMV
-# one-launch kernel: batch <= 8 with the activation slices in LDS and at most
-# 2 x 256 row tiles; the K-group kernel otherwise ((5120, 5120, 16),
-# (64, 4096, 8), (17408, 2048, 1), (16416, 64, 1))
+# one-launch kernel (four wavefronts per row tile up to 64 K steps, else
+# eight): batch <= 8 with the activation slices in LDS and at most one
+# resident round of row tiles; the K-group kernel otherwise ((5120, 5120, 16),
+# (64, 4096, 8), (34816, 2048, 1))
 NV_GEMV_CASES = [(512, 512, 1), (100, 96, 3), (33, 1040, 2), (7168, 5120, 1), (5120, 17408, 1), (5120, 5120, 16),
-                 (12288, 4096, 4), (64, 4096, 8), (17408, 2048, 1), (16416, 64, 1), (16384, 208, 8), (40, 16, 1)]
+                 (12288, 4096, 4), (64, 4096, 8), (17408, 2048, 1), (34816, 2048, 1), (16384, 208, 8), (40, 16, 1)]
 
 
 @pytest.mark.parametrize("N,K,B", NV_GEMV_CASES)
