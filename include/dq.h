@@ -262,9 +262,10 @@ dq_status dq_autocast_lut_to_nvfp4(const dq_lut_t* W, const float* G_override, c
  * x: device bf16 [B, K] row-major, 1 <= B <= 16.  W: NVFP4 weights as packed
  * by dq_pack_nvfp4 (rows = N, cols = K).  out_kind DQ_OUT_F32 / DQ_OUT_BF16:
  * y is device [B, N] row-major; x 16-byte aligned.  Small batches (B <= 8,
- * at most 2 row tiles of 32 per compute unit, B * K within the staging
- * limit) run in one launch that splits K inside each workgroup and needs no
- * workspace (dq_decode_gemv_nvfp4_workspace_size reports 0); otherwise
+ * row tiles of 32 that fit one resident round of workgroups, B * K within
+ * the staging limit) run in one launch that splits K inside each workgroup
+ * and needs no workspace (dq_decode_gemv_nvfp4_workspace_size reports 0);
+ * otherwise
  * workspace / workspace_bytes are as for dq_decode_gemv (partial sums over K
  * groups; NULL takes stream-ordered memory from the library's pool).
  * Activations are staged as fp16 after a power-of-two rescale per batch row
