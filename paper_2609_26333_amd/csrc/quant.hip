@@ -7,6 +7,8 @@
 // elements with fully coalesced 16-byte loads (8 lanes per row), computes the
 // per-16 block maxima with one cross-lane exchange, and writes the 1 KiB code
 // tile and 128-byte scale tile with contiguous stores.
+#include <type_traits>
+
 #include "dq_device.hpp"
 #include "dq_internal.hpp"
 
@@ -150,26 +152,51 @@ __global__ __launch_bounds__(256) void quantize_tiles_kernel(const T* __restrict
   const bool col_ok = col < cols;
   uint32_t* code_tile = reinterpret_cast<uint32_t*>(codes + tile * 1024);
   uint8_t* scale_tile = scales + tile * 128;
+  // all four row groups' loads first, unconditional from clamped in-bounds
+  // addresses (a load under a divergent branch is waited for inside it), then
+  // values outside the tensor are masked to zero: one memory round trip per
+  // wavefront
+  float v[4][8];
+  if constexpr (std::is_same<T, uint16_t>::value) {
+    const int64_t cc = min(col, cols - 8);   // cols % 16 == 0
+    uint4_t w[4];
+    float iv[4];
+    bool ok[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t row = tr * 32 + 8 * i + (lane >> 3);
+      const int64_t rc = min(row, rows - 1);
+      ok[i] = col_ok && row < rows;
+      w[i] = *reinterpret_cast<const uint4_t*>(x + rc * cols + cc);
+      if constexpr (NORM) iv[i] = inv[rc];
+    }
+    uint4_t gw{0u, 0u, 0u, 0u};
+    if constexpr (NORM) gw = *reinterpret_cast<const uint4_t*>(gamma + cc);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float lo = bf16_lo(w[i][j]), hi = bf16_hi(w[i][j]);
+        if constexpr (NORM) {   // two roundings, in this order
+          lo = (lo * iv[i]) * bf16_lo(gw[j]);
+          hi = (hi * iv[i]) * bf16_hi(gw[j]);
+        }
+        v[i][2 * j] = ok[i] ? lo : 0.0f;
+        v[i][2 * j + 1] = ok[i] ? hi : 0.0f;
+      }
+  } else {
+    static_assert(!NORM, "the normalizing quantizer takes bf16 activations");
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t row = tr * 32 + 8 * i + (lane >> 3);
+      load8(x, cols, row, col, col_ok && row < rows, v[i]);
+    }
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int r = 8 * i + (lane >> 3);
-    const int64_t row = tr * 32 + r;
-    float v[8];
-    load8(x, cols, row, col, col_ok && row < rows, v);
-    if constexpr (NORM) {
-      if (col_ok && row < rows) {
-        const float iv = inv[row];
-        float g[8];
-        load8(gamma, 0, 0, col, true, g);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float t = v[j] * iv;   // two roundings, in this order
-          v[j] = t * g[j];
-        }
-      }
-    }
     uint32_t sc;
-    const uint32_t w = quantize8(v, G, sc);
+    const uint32_t w = quantize8(v[i], G, sc);
     code_tile[r * 8 + c] = w;
     if ((c & 1) == 0) scale_tile[r * 4 + (c >> 1)] = (uint8_t)sc;
   }
