@@ -1,32 +1,33 @@
 #!/usr/bin/env python3
 """Benchmark of the phase-specific quantized linear layer on one MI355X.
 
-Workload: the 8B-scale MLP up-projection (Qwen3-8B shape: K = d_model = 4096,
-N = d_ffn x 3 = 12288), prefill M = 2048 tokens with 0.5 % outlier channels
-x30, decode batches 1 and 4; weights 0.02 N(0,1) with a log-normal row scale.
-Inputs are seeded synthetic tensors already resident in HBM.
+Workload (the largest single-GPU one): the decode-heavy sweep over 64
+stacked 27B-class blocks plus an NVFP4 prefill at M = 32768 tokens.
 
-One step = the whole per-token hot path over one batch:
-  1. NVFP4 activation quantization of X [2048, 4096] (static global scale),
-  2. W4A4 NVFP4 GEMM -> bf16 Y [2048, 12288],
-  3. LUT3 decode GEMV at batch 1 and at batch 4 (fp32 y).
-Weight packing (NVFP4 and per-row LUT3) is offline and timed separately.
+* Prefill: NVFP4 activation quantization (static global scale from a
+  calibration batch) of X [32768, 17408] bf16, then the W4A4 NVFP4 GEMM with
+  the 27B MLP down-projection W [5120, 17408] -> bf16 Y [32768, 5120].
+* Decode: one token through 64 stacked 27B blocks (q/k/v 7168x5120, o
+  5120x5120, gate/up 34816x5120, down 5120x17408; one packed block copied to
+  64 distinct buffers: 7.98 GB in LUT3, 5.31 GB in LUT2, far beyond the 256 MB
+  Infinity Cache) at batch 1, 8 and 16, in LUT3 and in LUT2 (per-row fp16
+  tables).  Each (format, batch) token is one captured HIP graph of 256
+  GEMV launches, replayed.
+Weights 0.02 N(0,1) times a log-normal row scale; activations N(0,1) with
+0.5 % outlier channels x30 (seeded synthetic tensors, resident in HBM).
 
-The decode weights of a step rotate over enough packed copies (>= 768 MiB)
-that every GEMV streams its weights from HBM rather than from the 256 MiB
-Infinity Cache; the activations X rotate over 16 copies for the same reason.
-
-Besides the step, the run measures a decode sweep outside the timed steps:
-one decode token through 64 stacked 27B-class blocks (q/k/v 7168x5120,
-o 5120x5120, gate/up 34816x5120, down 5120x17408: 7.93 GB of LUT3 codes, all
-distinct memory) at batch 1, 8 and 16, and the same in LUT2 at batch 1.
-
-Prints one JSON line.  `ms_per_step` is the time of the timed steps (HIP
-events on the launch stream around them, nothing else in between).  `value`
-is the prefill linear throughput: 2*M*N*K over (quantization + GEMM) time,
-each measured as back-to-back calls of that kernel alone between one pair of
-events (the average includes the GPU-side gap between launches, no host or
-event overhead); the GEMV rates are measured the same way.
+One step = prefill quantization + GEMM + the six decode tokens.  The run
+does `warmup` steps, then times `steps` steps between two HIP events on the
+launch stream (`ms_per_step`); HIP events between the phases of every timed
+step give each phase's average duration.  `value` is the prefill linear's
+throughput 2*M*N*K / (quantization + GEMM); `roofline` is the GEMM kernel
+against the dense FP4 peak (its fp16-MFMA fraction alongside), and
+`roofline_decode` the LUT3 batch-1 token against HBM.  Outside the timed
+steps the run also measures the 27B down-projection at M = 8192 with fused
+activation quantization, the 27B block chained at M = 4096 with NVFP4
+epilogues, the MXFP4 variant of the prefill GEMM, the NVFP4A16 decode GEMV,
+the engine clock under GEMM and GEMV load, and the CPU oracle on a bounded
+sample of the same workload.
 
 `--calibrate-copy` instead runs a plain 256 MiB device copy five times: the
 reference kernel whose FETCH_SIZE / WRITE_SIZE readings scale the GEMM's
@@ -38,7 +39,9 @@ import hashlib
 import json
 import os
 import re
+import subprocess
 import sys
+import tempfile
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -48,22 +51,42 @@ METRIC = "NVFP4 prefill GEMM TFLOPS (%FP4 peak); LUT3 decode GEMV GB/s (%HBM pea
 PEAK_FP16_TFLOPS = 2500.0      # dense fp16/bf16 MFMA, MI355X
 PEAK_FP4_TFLOPS = 10100.0      # dense fp4 MFMA, MI355X
 PEAK_HBM_GBS = 8000.0
-# sources that decide the GEMM's kernels and launches (tile geometry, column split)
+# sources that decide the GEMM's kernels and launches
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2609_26333_amd", "csrc", f) for f in ("gemm.hip", "dq_internal.hpp")]
-GEMM_COUNTERS = os.path.join(ROOT, "profiles", "nvfp4_gemm_8b_up_proj_counters.md")
+GEMM_COUNTERS = os.path.join(ROOT, "profiles", "nvfp4_gemm_27b_down_m32768_counters.md")
 COPY_BYTES = 256 << 20
+SWEEP = ((3, 1), (3, 8), (3, 16), (2, 1), (2, 8), (2, 16))
+
+# Clock sampler: a separate process, started before this one touches the GPU,
+# that appends amd-smi's per-XCD graphics clocks with a timestamp to a file.
+SAMPLER = r"""
+import json, subprocess, sys, time
+out = sys.argv[1]
+while True:
+    t = time.time()
+    try:
+        r = subprocess.run(["amd-smi", "metric", "-c", "--json"], capture_output=True, text=True, timeout=20)
+        d = json.loads(r.stdout)
+        clk = d["gpu_data"][0]["clock"] if "gpu_data" in d else d[0]["clock"]
+        v = [c["clk"]["value"] for k, c in clk.items() if k.startswith("gfx_") and isinstance(c.get("clk"), dict)]
+        rec = {"t0": t, "t1": time.time(), "gfx_mhz": v}
+    except Exception as e:
+        rec = {"t0": t, "t1": time.time(), "error": str(e)[:200]}
+    with open(out, "a") as f:
+        f.write(json.dumps(rec) + "\n")
+    time.sleep(0.05)
+"""
 
 
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--no-decode-sweep", action="store_true")
+    p.add_argument("--no-extras", action="store_true", help="skip the measurements outside the timed steps")
+    p.add_argument("--no-sclk", action="store_true")
     p.add_argument("--sweep-blocks", type=int, default=64)
-    p.add_argument("--decode-bytes", type=int, default=768 << 20,
-                   help="total bytes of rotated decode weight copies")
     p.add_argument("--calibrate-copy", action="store_true")
     return p.parse_args()
 
@@ -76,12 +99,10 @@ def gemm_source_sha256():
 
 
 def gemm_traffic():
-    """HBM bytes per GEMM call from the committed counter summary: the
-    FETCH_SIZE and WRITE_SIZE readings of the call's kernel launches (a
-    full-tile launch and, for a partial last round, a half-width-tile launch),
-    each scaled by the bytes a plain copy of known size moves per KiB that the
-    same counter reads.  None when the summary is missing or the GEMM sources
-    have changed since."""
+    """HBM bytes per GEMM call from the committed counter summary: FETCH_SIZE
+    and WRITE_SIZE of the GEMM kernel, each scaled by the bytes a plain copy
+    of known size moves per KiB that the same counter reads.  None when the
+    summary is missing or the GEMM sources have changed since."""
     try:
         text = open(GEMM_COUNTERS).read()
     except OSError:
@@ -109,170 +130,65 @@ def calibrate_copy():
                       "launches": 5}), flush=True)
 
 
-def cpu_baseline(cfg, w, X, G_x, xds, min_seconds=10.0):
-    """Time the CPU oracle on the same workload: the whole prefill layer
-    (activation quantization + fp64 GEMM over the dequantized operands) and
-    the batch-1 and batch-4 LUT3 GEMVs, repeated until min_seconds have
-    passed.  Weight packing is offline and untimed."""
+def clock_window(path, t0, t1):
+    """Median per-XCD graphics clock (MHz) of the samples taken inside [t0, t1]."""
+    if path is None or not os.path.exists(path):
+        return None
+    vals = []
+    for line in open(path):
+        try:
+            r = json.loads(line)
+        except ValueError:
+            continue
+        if "gfx_mhz" in r and r["t0"] >= t0 and r["t1"] <= t1:
+            vals += r["gfx_mhz"]
+    if not vals:
+        return None
+    vals.sort()
+    return {"median_mhz": vals[len(vals) // 2], "min_mhz": vals[0], "max_mhz": vals[-1], "readings": len(vals)}
+
+
+def cpu_baseline(w_down, X, G_x, min_seconds=10.0):
+    """The CPU oracle on a bounded sample of the same workload, repeated until
+    min_seconds have passed: the prefill linear for 32 of the 32768 token rows
+    (NVFP4 quantization + fp64 GEMM against all 5120 weight rows) and the
+    batch-1 LUT3 GEMV of one block's down-projection (dequantization + fp64
+    GEMV).  Weight packing is offline and untimed."""
+    import numpy as np
     from threadpoolctl import threadpool_info
 
+    import synth
     from oracle import linalg, lut, nvfp4
-    qw, cw, Gw = nvfp4.quantize_dynamic(w)
-    codes, table = lut.quantize_per_row(w, 3)
+    cfg = synth.CONFIGS[4]
+    qw, cw, Gw = nvfp4.quantize_dynamic(w_down)
     w_hat = nvfp4.dequantize(qw, cw, Gw)
-    M, K = X.shape
-    N = w.shape[0]
+    codes, table = lut.quantize_per_row(w_down, 3)
+    xd = synth.decode_x(cfg, w_down.shape[1], 1)
+    rows = 32
+    Xs = X[:rows]
+    N, K = w_down.shape
     t_pre = t_dec = 0.0
     reps = 0
     start = time.perf_counter()
     while reps == 0 or time.perf_counter() - start < min_seconds:
         t0 = time.perf_counter()
-        qa, ca, _ = nvfp4.quantize_bf16_activations(X, G_x)
-        Y = linalg.gemm(nvfp4.dequantize(qa, ca, G_x), w_hat)
+        qa, ca, _ = nvfp4.quantize_bf16_activations(Xs, G_x)
+        linalg.gemm(nvfp4.dequantize(qa, ca, G_x), w_hat)
         t1 = time.perf_counter()
-        for xd in xds.values():
-            linalg.lut_gemv_per_row(xd, codes, table)
+        linalg.lut_gemv_per_row(xd, codes, table)
         t_pre += t1 - t0
         t_dec += time.perf_counter() - t1
         reps += 1
-        del Y
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    dec_bytes = sum(N * K * 3 / 8 + N * 16 + xd.size * 2 + xd.shape[0] * N * 4 for xd in xds.values())
+    dec_bytes = N * K * 3 / 8 + N * 16 + K * 2 + N * 4
     return {
-        "value": 2.0 * M * N * K * reps / t_pre / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-        "sample": (f"the whole layer {reps} times: NVFP4 quantization of X[{M},{K}] + fp64 GEMM against all "
-                   f"{N} weight rows ({t_pre / reps:.2f} s each); decode: LUT3 dequantization + fp64 GEMV at "
-                   f"batch {' and '.join(str(b) for b in xds)} ({t_dec / reps:.2f} s each, "
-                   f"{dec_bytes * reps / t_dec / 1e9:.3f} GB/s); weight packing untimed"),
+        "value": 2.0 * rows * N * K * reps / t_pre / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+        "sample": (f"prefill linear for {rows} of the 32768 token rows (NVFP4 quantization of X[{rows},{K}] + fp64 "
+                   f"GEMM against all {N} weight rows), {reps} times, {t_pre / reps:.2f} s each; decode: LUT3 "
+                   f"dequantization + fp64 GEMV of one 27B down-projection ({N}x{K}) at batch 1, "
+                   f"{t_dec / reps:.2f} s each = {dec_bytes * reps / t_dec / 1e9:.3f} GB/s; packing untimed"),
         "decode_gbps": dec_bytes * reps / t_dec / 1e9,
     }
-
-
-def mxfp4_prefill(dq, torch, np, w, Xs, M, N, K, s, reps):
-    """The MXFP4 W4A4 variant of the same prefill linear (OCP MX: E8M0 scale
-    per 32, block scales applied inside the FP4 MFMA), timed apart from the
-    NVFP4 steps: activation quantization and GEMM with HIP events around
-    `reps` calls of each."""
-    lib = dq.lib()
-    sp = ctypes.c_void_p(s.cuda_stream)
-    Wm = dq.dq_pack_mxfp4(torch.from_numpy(np.ascontiguousarray(w)).cuda())
-    A = dq.MxFp4Tensor.empty(M, K)
-    Y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-    dA, dW = A.desc(), Wm.desc()
-    n_x = len(Xs)
-
-    def quant(i):
-        return lib.dq_quantize_act_mxfp4(ctypes.c_void_p(Xs[i % n_x].data_ptr()), M, K, ctypes.byref(dA), sp)
-
-    def gemm():
-        return lib.dq_prefill_gemm_mxfp4(ctypes.byref(dA), ctypes.byref(dW), dq.OUT_BF16,
-                                         ctypes.c_void_p(Y.data_ptr()), sp)
-    for i in range(3):
-        assert quant(i) == 0 and gemm() == 0
-    torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-    ev[0].record(s)
-    for i in range(reps):
-        assert quant(i) == 0
-    ev[1].record(s)
-    for _ in range(reps):
-        assert gemm() == 0
-    ev[2].record(s)
-    torch.cuda.synchronize()
-    t_q = ev[0].elapsed_time(ev[1]) / reps * 1e-3
-    t_g = ev[1].elapsed_time(ev[2]) / reps * 1e-3
-    flops = 2.0 * M * N * K
-    return {"quant_us": t_q * 1e6, "quant_GB/s": M * K * (2 + 0.5 + 1 / 32) / t_q / 1e9,
-            "gemm_us": t_g * 1e6, "gemm_TFLOP/s": flops / t_g / 1e12,
-            "frac_fp4_peak": flops / t_g / 1e12 / PEAK_FP4_TFLOPS,
-            "linear_TFLOP/s_incl_quant": flops / (t_q + t_g) / 1e12,
-            "note": "MXFP4 W4A4 (E2M1, E8M0 per 32 along K) on the scaled FP4 MFMA; same shapes and bf16 output"}
-
-
-def nvfp4a16_decode(dq, torch, np, Wq, xd_dev, Bs, N, K, s, decode_bytes, reps):
-    """Weight-only NVFP4 decode GEMV (format-disaggregated NVFP4) over the same
-    packed NVFP4 weights the prefill GEMM uses, at the decode batches, with
-    the weights rotated over enough copies to stream from HBM."""
-    lib = dq.lib()
-    sp = ctypes.c_void_p(s.cuda_stream)
-    nbytes = Wq.codes.numel() + Wq.scales.numel()
-    n_w = max(2, -(-decode_bytes // nbytes))
-    Ws = [Wq] + [dq.NvFp4Tensor(Wq.codes.clone(), Wq.scales.clone(), Wq.G.clone(), N, K) for _ in range(n_w - 1)]
-    ds = [x.desc() for x in Ws]
-    out = {}
-    for b in Bs:
-        y = torch.empty((b, N), dtype=torch.float32, device="cuda")
-        ws_n = dq.dq_decode_gemv_nvfp4_workspace_size(b, Wq)
-        ws = torch.empty(max(ws_n, 16), dtype=torch.uint8, device="cuda")
-        args_ = (ctypes.c_void_p(xd_dev[b].data_ptr()), b)
-        call = lambda i: lib.dq_decode_gemv_nvfp4(*args_, ctypes.byref(ds[i % n_w]), dq.OUT_F32,  # noqa: E731
-                                                 ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
-                                                 ws_n, sp)
-        for i in range(n_w):
-            assert call(i) == 0
-        torch.cuda.synchronize()
-        ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ea.record(s)
-        for i in range(reps):
-            call(i)
-        eb.record(s)
-        torch.cuda.synchronize()
-        t = ea.elapsed_time(eb) / reps * 1e-3
-        alg = nbytes + b * K * 2 + b * N * 4
-        out[f"b{b}"] = {"us": t * 1e6, "GB/s": alg / t / 1e9, "frac_hbm": alg / t / 1e9 / PEAK_HBM_GBS,
-                        "bytes": alg}
-    out["weight_copies"] = n_w
-    out["note"] = "NVFP4 weights (4.5 bits), bf16 x, fp16 MFMA; back-to-back calls; one launch per call at these batches (K split inside each workgroup)"
-    return out
-
-
-def decode_sweep(dq, synth, torch, np, n_blocks, steps):
-    """One decode token through n_blocks stacked 27B-class blocks (distinct
-    copies of one packed block), LUT3 at batch 1, 8, 16 and LUT2 at batch 1."""
-    cfg = synth.CONFIGS[4]
-    lib = dq.lib()
-    s = torch.cuda.current_stream()
-    sp = ctypes.c_void_p(s.cuda_stream)
-    out = {}
-    Ws = [torch.from_numpy(synth.layer_weight(cfg, layer)).cuda() for layer in cfg.layers]
-    for bits, batches in ((3, (1, 8, 16)), (2, (1,))):
-        block = [dq.dq_pack_lut3(W, bits=bits, mode=dq.LUT_PER_ROW) for W in Ws]
-        if bits == 2:
-            del Ws
-        stack = [block] + [[dq.LutWeight(l.codes.clone(), l.lut.clone(), None, None, l.rows, l.cols, bits,
-                                         dq.LUT_PER_ROW) for l in block] for _ in range(n_blocks - 1)]
-        descs = [[l.desc() for l in blk] for blk in stack]
-        wbytes = sum(l.codes.numel() + l.lut.numel() * 2 for blk in stack for l in blk)
-        for B in batches:
-            xs = [torch.from_numpy(synth.decode_x(cfg, l.k, B).view(np.int16)).cuda() for l in cfg.layers]
-            ys = [torch.empty((B, l.n), dtype=torch.float32, device="cuda") for l in cfg.layers]
-            xp = [ctypes.c_void_p(t.data_ptr()) for t in xs]
-            yp = [ctypes.c_void_p(t.data_ptr()) for t in ys]
-            ws_n = max(dq.dq_decode_gemv_workspace_size(B, l) for l in block)
-            ws = torch.empty(max(ws_n, 16), dtype=torch.uint8, device="cuda")
-            wsp = ctypes.c_void_p(ws.data_ptr())
-
-            def token():
-                for d in descs:
-                    for i in range(len(cfg.layers)):
-                        assert lib.dq_decode_gemv(xp[i], B, ctypes.byref(d[i]), dq.OUT_F32, yp[i], wsp, ws_n,
-                                                  sp) == 0
-            token()
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(s)
-            for _ in range(steps):
-                token()
-            e1.record(s)
-            torch.cuda.synchronize()
-            t = e0.elapsed_time(e1) / steps * 1e-3
-            io = n_blocks * sum(B * l.k * 2 + B * l.n * 4 for l in cfg.layers)
-            gbs = (wbytes + io) / t / 1e9
-            out[f"lut{bits}_b{B}"] = {"ms_per_token": t * 1e3, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
-                                      "weight_bytes": wbytes, "gemv_launches": n_blocks * len(cfg.layers)}
-        del stack, descs, block
-        torch.cuda.empty_cache()
-    return out
 
 
 def main():
@@ -284,6 +200,24 @@ def main():
     if args.calibrate_copy:
         calibrate_copy()
         return
+    sampler = clk_path = None
+    if not args.no_sclk:
+        clk_path = os.path.join(tempfile.mkdtemp(prefix="dq_clk_"), "clk.jsonl")
+        try:
+            sampler = subprocess.Popen([sys.executable, "-c", SAMPLER, clk_path], stdout=subprocess.DEVNULL,
+                                       stderr=subprocess.DEVNULL)
+        except OSError:
+            sampler = clk_path = None
+    try:
+        out = run(args, clk_path)
+    finally:
+        if sampler is not None:
+            sampler.kill()
+            sampler.wait()
+    print(json.dumps(out), flush=True)
+
+
+def run(args, clk_path):
     import numpy as np
     import torch
 
@@ -292,182 +226,309 @@ def main():
 
     torch.cuda.set_device(0)
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()   # noqa: E731
-    cfg = synth.CONFIGS[1]
-    layer = cfg.layers[0]
-    M, N, K = cfg.m, layer.n, layer.k
-    Bs = cfg.decode_batches
-
-    w = synth.layer_weight(cfg, layer)
-    X = synth.prefill_x(cfg, K)
-    calib = synth.prefill_x(cfg, K, calib=True)
-    xds = {b: synth.decode_x(cfg, K, b) for b in Bs}
-
-    W_dev = dev(w)
+    lib = dq.lib()
     s = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    Wq = dq.dq_pack_nvfp4(W_dev)
-    e1.record()
-    torch.cuda.synchronize()
-    t_pack_nvfp4 = e0.elapsed_time(e1)
-    e0.record()
-    Wl = dq.dq_pack_lut3(W_dev, bits=3, mode=dq.LUT_PER_ROW)
-    e1.record()
-    torch.cuda.synchronize()
-    t_pack_lut = e0.elapsed_time(e1)
-    del W_dev
-    # LUT -> NVFP4 autocast of the packed LUT3 weight (the prefill view of a LUT model), once warm
-    dq.dq_autocast_lut_to_nvfp4(Wl)
-    torch.cuda.synchronize()
-    e0.record()
-    Wac = dq.dq_autocast_lut_to_nvfp4(Wl)
-    e1.record()
-    torch.cuda.synchronize()
-    t_autocast = e0.elapsed_time(e1)
-    del Wac
+    sp = ctypes.c_void_p(s.cuda_stream)
+    ev = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
 
-    # static activation scale from a calibration batch (running-max observer stand-in)
-    A_cal = dq.dq_quantize_act_nvfp4(dev(calib.view(np.int16)))
-    G_x = A_cal.G.clone()
-    torch.cuda.synchronize()
-    G_x_host = float(G_x.cpu()[0])
-
-    # rotation buffers
-    n_x = 16
-    Xs = [dev(X.view(np.int16)) for _ in range(n_x)]
-    lut_bytes = Wl.codes.numel() + Wl.lut.numel() * 2
-    n_w = max(2, -(-args.decode_bytes // lut_bytes))
-    Wls = [Wl] + [dq.LutWeight(Wl.codes.clone(), Wl.lut.clone(), None, None, N, K, 3, dq.LUT_PER_ROW)
-                  for _ in range(n_w - 1)]
-    xd_dev = {b: dev(xds[b].view(np.int16)) for b in Bs}
+    # ---------------------------------------------------------------- prefill inputs
+    cfg = synth.CONFIGS[4]
+    layers = {l.name: l for l in cfg.layers}
+    down = layers["down"]
+    M, N, K = cfg.m, down.n, down.k
+    w_down = synth.layer_weight(cfg, down)
+    Wq = dq.dq_pack_nvfp4(dev(w_down))
+    X_host = synth.prefill_x(cfg, K)
+    X = dev(X_host.view(np.int16))
+    calib = dev(synth.prefill_x(cfg, K, m=2048, calib=True).view(np.int16))
+    G_x = dq.dq_quantize_act_nvfp4(calib).G.clone()   # static scale: the dynamic rule on the calibration batch
+    del calib
     A = dq.NvFp4Tensor.empty(M, K)
     Y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-    ys = {b: torch.empty((b, N), dtype=torch.float32, device="cuda") for b in Bs}
-
-    # prebuilt raw C-ABI calls (keeps host enqueue far ahead of the GPU)
-    lib = dq.lib()
-    sp = ctypes.c_void_p(s.cuda_stream)
     dA, dW = A.desc(), Wq.desc()
-    dWls = [x.desc() for x in Wls]
     gx = ctypes.c_void_p(G_x.data_ptr())
 
-    def quant(i):
-        return lib.dq_quantize_act_nvfp4(ctypes.c_void_p(Xs[i % n_x].data_ptr()), M, K, gx, ctypes.byref(dA), sp)
+    def quant():
+        assert lib.dq_quantize_act_nvfp4(ctypes.c_void_p(X.data_ptr()), M, K, gx, ctypes.byref(dA), sp) == 0
 
     def gemm():
-        return lib.dq_prefill_gemm(ctypes.byref(dA), None, None, ctypes.byref(dW), M, dq.OUT_BF16,
-                                   ctypes.c_void_p(Y.data_ptr()), None, None, 0, sp)
+        assert lib.dq_prefill_gemm(ctypes.byref(dA), None, None, ctypes.byref(dW), M, dq.OUT_BF16,
+                                   ctypes.c_void_p(Y.data_ptr()), None, None, 0, None, 0, sp) == 0
 
-    ws_n = max(dq.dq_decode_gemv_workspace_size(b, Wls[0]) for b in Bs)
-    ws = torch.empty(max(ws_n, 16), dtype=torch.uint8, device="cuda")
-    wsp = ctypes.c_void_p(ws.data_ptr())
+    # ---------------------------------------------------------------- decode sweep
+    Ws = {l.name: dev(synth.layer_weight(cfg, l)) for l in cfg.layers}
+    stacks, wbytes = {}, {}
+    for bits in (3, 2):
+        block = [dq.dq_pack_lut3(Ws[l.name], bits=bits, mode=dq.LUT_PER_ROW) for l in cfg.layers]
+        stacks[bits] = [block] + [[dq.LutWeight(w.codes.clone(), w.lut.clone(), None, None, w.rows, w.cols, bits,
+                                                dq.LUT_PER_ROW) for w in block] for _ in range(args.sweep_blocks - 1)]
+        wbytes[bits] = sum(w.codes.numel() + w.lut.numel() * 2 for blk in stacks[bits] for w in blk)
+    del Ws
+    torch.cuda.empty_cache()
+    xs = {B: [dev(synth.decode_x(cfg, l.k, B).view(np.int16)) for l in cfg.layers] for B in (1, 8, 16)}
+    ys = {B: [torch.empty((B, l.n), dtype=torch.float32, device="cuda") for l in cfg.layers] for B in (1, 8, 16)}
+    graphs, keep = {}, []
+    cap = torch.cuda.Stream()
+    for bits, B in SWEEP:
+        descs = [[w.desc() for w in blk] for blk in stacks[bits]]
+        ws_n = max(dq.dq_decode_gemv_workspace_size(B, w) for w in stacks[bits][0])
+        ws = torch.empty(max(ws_n, 16), dtype=torch.uint8, device="cuda")
+        keep += [descs, ws]
 
-    def gemv(i, b):
-        return lib.dq_decode_gemv(ctypes.c_void_p(xd_dev[b].data_ptr()), b, ctypes.byref(dWls[i % n_w]),
-                                  dq.OUT_F32, ctypes.c_void_p(ys[b].data_ptr()), wsp, ws_n, sp)
-
-    def step(i):
-        assert quant(i) == 0
-        assert gemm() == 0
-        for j, b in enumerate(Bs):
-            assert gemv(i * len(Bs) + j, b) == 0
-
-    for i in range(args.warmup):
-        step(i)
+        def token(stream, descs=descs, B=B, ws=ws, ws_n=ws_n):
+            p = ctypes.c_void_p(stream.cuda_stream)
+            for d in descs:
+                for i in range(len(cfg.layers)):
+                    assert lib.dq_decode_gemv(ctypes.c_void_p(xs[B][i].data_ptr()), B, ctypes.byref(d[i]), dq.OUT_F32,
+                                              ctypes.c_void_p(ys[B][i].data_ptr()), ctypes.c_void_p(ws.data_ptr()),
+                                              ws_n, p) == 0
+        token(s)            # warm: kernel attributes and plans are set up outside the capture
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cap):
+            token(torch.cuda.current_stream())
+        graphs[(bits, B)] = g
     torch.cuda.synchronize()
-    # the timed steps: nothing but the step's launches between the two events
-    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    # ---------------------------------------------------------------- timed steps
+    n_ph = 2 + len(SWEEP)
+
+    def step(marks):
+        marks[0].record(s)
+        quant()
+        marks[1].record(s)
+        gemm()
+        marks[2].record(s)
+        for j, key in enumerate(SWEEP):
+            graphs[key].replay()
+            marks[3 + j].record(s)
+
+    for _ in range(args.warmup):
+        step([ev() for _ in range(n_ph + 1)])
+    torch.cuda.synchronize()
+    marks = [[ev() for _ in range(n_ph + 1)] for _ in range(args.steps)]
+    t_start, t_end = ev(), ev()
     t_start.record(s)
     for i in range(args.steps):
-        step(args.warmup + i)
+        step(marks[i])
     t_end.record(s)
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
-
-    # per-kernel rates: `reps` back-to-back calls of one kernel (rotating the
-    # activation copies and decode weight copies) between one pair of events,
-    # so the average includes the GPU-side gap between launches but no event
-    # or host overhead
-    reps = max(20, args.steps)
-
-    def back_to_back(fn):
-        for i in range(3):
-            fn(i)
-        torch.cuda.synchronize()
-        ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ea.record(s)
-        for i in range(reps):
-            fn(i)
-        eb.record(s)
-        torch.cuda.synchronize()
-        return ea.elapsed_time(eb) / reps
-
-    per = {"quant": back_to_back(lambda i: quant(i)), "gemm": back_to_back(lambda i: gemm())}
-    # the same quantizer fused with the RMSNorm that precedes the projection
-    gamma = dev(synth.bf16_bits_from_f32((1.0 + 0.2 * synth.random_f32(7, (1, K))).astype(np.float32))[0]
-                .view(np.int16))
-
-    norm_ws = torch.empty(4 * M, dtype=torch.uint8, device="cuda")
-
-    def norm_quant(i):
-        return lib.dq_rmsnorm_quantize_act_nvfp4(ctypes.c_void_p(Xs[i % n_x].data_ptr()),
-                                                 ctypes.c_void_p(gamma.data_ptr()), ctypes.c_float(1e-6), M, K, gx,
-                                                 ctypes.byref(dA), ctypes.c_void_p(norm_ws.data_ptr()), 4 * M, sp)
-    per["norm_quant"] = back_to_back(norm_quant)
-    for b in Bs:
-        per[f"gemv_b{b}"] = back_to_back(lambda i, b=b: gemv(i, b))
+    ph = [sum(m[j].elapsed_time(m[j + 1]) for m in marks) / args.steps for j in range(n_ph)]   # ms
+    t_quant, t_gemm = ph[0] * 1e-3, ph[1] * 1e-3
 
     flops = 2.0 * M * N * K
+    gemm_tflops = flops / t_gemm / 1e12
+    prefill_tflops = flops / (t_quant + t_gemm) / 1e12
     quant_bytes = M * K * 2 + M * K / 2 + M * K / 16
-    gemm_tflops = flops / (per["gemm"] * 1e-3) / 1e12
-    prefill_tflops = flops / ((per["quant"] + per["gemm"]) * 1e-3) / 1e12
     decode = {}
-    for b in Bs:
-        nbytes = N * K * 3 / 8 + N * 8 * 2 + b * K * 2 + b * N * 4
-        gbs = nbytes / (per[f"gemv_b{b}"] * 1e-3) / 1e9
-        decode[f"b{b}"] = {"us": per[f"gemv_b{b}"] * 1e3, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
-                           "bytes": nbytes}
-    # algorithmic bytes of one GEMM call: the NVFP4 operands once, the bf16 output once
+    io = {B: args.sweep_blocks * sum(B * l.k * 2 + B * l.n * 4 for l in cfg.layers) for B in (1, 8, 16)}
+    for j, (bits, B) in enumerate(SWEEP):
+        t = ph[2 + j] * 1e-3
+        gbs = (wbytes[bits] + io[B]) / t / 1e9
+        decode[f"lut{bits}_b{B}"] = {"ms_per_token": t * 1e3, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
+                                     "bytes": wbytes[bits] + io[B],
+                                     "gemv_launches": args.sweep_blocks * len(cfg.layers)}
     gemm_alg_bytes = M * K * (0.5 + 1 / 16) + N * K * (0.5 + 1 / 16) + M * N * 2
     traffic = gemm_traffic()
-
     out = {
         "metric": METRIC, "value": prefill_tflops, "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": total_ms / args.steps,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
         "data": "synthetic",
-        "config": {"workload": "8B-scale MLP up-projection: K=4096, N=12288, prefill M=2048 (NVFP4 W4A4), "
-                               "decode B=1,4 (LUT3 per-row fp16 tables)",
-                   "M": M, "N": N, "K": K, "decode_batches": list(Bs), "static_G_x": G_x_host,
-                   "decode_weight_copies": n_w, "x_copies": n_x},
-        "prefill": {"quant_us": per["quant"] * 1e3, "quant_GB/s": quant_bytes / (per["quant"] * 1e-3) / 1e9,
-                    "rmsnorm_quant_us": per["norm_quant"] * 1e3,
-                    "gemm_us": per["gemm"] * 1e3, "gemm_TFLOP/s": gemm_tflops,
-                    "frac_fp16_mfma_peak": gemm_tflops / PEAK_FP16_TFLOPS,
+        "config": {"workload": ("decode-heavy sweep over 64 stacked 27B-class blocks (LUT3 and LUT2 per-row "
+                                "tables, batch 1/8/16) plus NVFP4 prefill at M=32768 on the 27B down-projection "
+                                "(K=17408, N=5120)"),
+                   "M": M, "N": N, "K": K, "decode_batches": [1, 8, 16], "sweep_blocks": args.sweep_blocks,
+                   "static_G_x": float(G_x.cpu()[0]), "decode_tokens": "captured HIP graphs, 256 GEMVs each"},
+        "prefill": {"quant_us": t_quant * 1e6, "quant_GB/s": quant_bytes / t_quant / 1e9,
+                    "quant_frac_hbm": quant_bytes / t_quant / 1e9 / PEAK_HBM_GBS,
+                    "gemm_us": t_gemm * 1e6, "gemm_TFLOP/s": gemm_tflops,
                     "frac_fp4_peak": gemm_tflops / PEAK_FP4_TFLOPS,
+                    "frac_fp16_mfma_peak": gemm_tflops / PEAK_FP16_TFLOPS,
                     "linear_TFLOP/s_incl_quant": prefill_tflops},
         "decode": decode,
-        "pack_ms": {"nvfp4": t_pack_nvfp4, "lut3_per_row": t_pack_lut, "lut3_to_nvfp4_autocast": t_autocast},
         "roofline": {"bound": "mfma", "kernel": "nvfp4_gemm_kernel (one launch per dq_prefill_gemm call)",
-                     "achieved": gemm_tflops,
-                     "peak": PEAK_FP16_TFLOPS, "unit": "TFLOP/s", "frac": gemm_tflops / PEAK_FP16_TFLOPS,
+                     "achieved": gemm_tflops, "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s",
+                     "frac": gemm_tflops / PEAK_FP4_TFLOPS,
+                     "frac_fp16_mfma": gemm_tflops / PEAK_FP16_TFLOPS,
                      "traffic": traffic,
                      "traffic_note": (f"HBM bytes per GEMM call from FETCH_SIZE + WRITE_SIZE (copy-calibrated); "
                                       f"algorithmic bytes {gemm_alg_bytes:.4g}" if traffic is not None else
-                                      "no counter summary for the current GEMM source"),
-                     "note": "exact NVFP4 operands are dequantized to fp16 and multiplied on fp16 MFMA; "
-                             "frac of the dense FP4 peak is prefill.frac_fp4_peak"},
+                                      f"no counter summary for the current GEMM source; algorithmic bytes "
+                                      f"{gemm_alg_bytes:.4g}"),
+                     "note": "exact NVFP4 (E4M3 scale per 16) runs on the fp16 MFMA after exact dequantization, "
+                             "whose dense peak is a quarter of the FP4 peak"},
+        "roofline_decode": {"bound": "hbm", "kernel": "LUT3 batch-1 token: 256 dq_decode_gemv launches",
+                            "achieved": decode["lut3_b1"]["GB/s"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                            "frac": decode["lut3_b1"]["frac_hbm"]},
     }
-    out["mxfp4_prefill"] = mxfp4_prefill(dq, torch, np, w, Xs, M, N, K, s, args.steps)
-    out["nvfp4a16_decode"] = nvfp4a16_decode(dq, torch, np, Wq, xd_dev, Bs, N, K, s, args.decode_bytes, reps)
-    del Wls, dWls, Xs
-    torch.cuda.empty_cache()
-    if not args.no_decode_sweep:
-        out["decode_sweep_27b_blocks"] = decode_sweep(dq, synth, torch, np, args.sweep_blocks, 5)
-        out["decode_sweep_27b_blocks"]["blocks"] = args.sweep_blocks
+    if not args.no_extras:
+        del graphs, keep
+        torch.cuda.synchronize()
+        out["sclk"] = measure_clocks(dq, torch, lib, s, sp, gemm, stacks, xs, ys, cfg, clk_path)
+        del stacks
+        torch.cuda.empty_cache()
+        out["mxfp4_prefill_m32768"] = mxfp4_prefill(dq, torch, lib, s, sp, w_down, X, M, N, K)
+        del A, Y, X
+        torch.cuda.empty_cache()
+        out["c2_fused_m8192"] = c2_fused(dq, synth, torch, np, lib, s, sp)
+        out["c3_block_chain_m4096"] = c3_chain(dq, synth, torch, np, lib, s, sp)
+        out["nvfp4a16_decode_27b_down"] = nvfp4a16_decode(dq, torch, lib, s, sp, Wq, N, K)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, w, X, np.float32(G_x_host), xds)
-    print(json.dumps(out), flush=True)
+        out["cpu_baseline"] = cpu_baseline(w_down, X_host, np.float32(out["config"]["static_G_x"]))
+    return out
+
+
+def timed(torch, s, fn, reps):
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    for _ in range(reps):
+        fn()
+    e1.record(s)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps * 1e-3
+
+
+def measure_clocks(dq, torch, lib, s, sp, gemm, stacks, xs, ys, cfg, clk_path):
+    """Engine clock while the GPU runs back-to-back prefill GEMMs (about 2 s)
+    and back-to-back LUT3 batch-1 GEMVs over the 64 blocks (about 2 s)."""
+    if clk_path is None:
+        return None
+    res = {}
+    gemm()
+    torch.cuda.synchronize()
+    t0 = time.time()
+    for _ in range(450):
+        gemm()
+    torch.cuda.synchronize()
+    res["prefill_gemm"] = clock_window(clk_path, t0, time.time())
+    descs = [[w.desc() for w in blk] for blk in stacks[3]]
+    t0 = time.time()
+    for _ in range(700):
+        for d in descs:
+            for i in range(len(cfg.layers)):
+                lib.dq_decode_gemv(ctypes.c_void_p(xs[1][i].data_ptr()), 1, ctypes.byref(d[i]), dq.OUT_F32,
+                                   ctypes.c_void_p(ys[1][i].data_ptr()), None, 0, sp)
+        if time.time() - t0 > 2.0:
+            break
+    torch.cuda.synchronize()
+    res["decode_gemv_lut3_b1"] = clock_window(clk_path, t0, time.time())
+    res["source"] = "amd-smi metric -c (per-XCD graphics clock), sampled by a helper process"
+    return res
+
+
+def mxfp4_prefill(dq, torch, lib, s, sp, w, X, M, N, K):
+    """The MXFP4 W4A4 variant of the same prefill linear (OCP MX: E8M0 scale
+    per 32, block scales applied inside the FP4 MFMA)."""
+    Wm = dq.dq_pack_mxfp4(torch.from_numpy(w).cuda())
+    A = dq.MxFp4Tensor.empty(M, K)
+    Y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    dA, dW = A.desc(), Wm.desc()
+    t_q = timed(torch, s, lambda: lib.dq_quantize_act_mxfp4(ctypes.c_void_p(X.data_ptr()), M, K, ctypes.byref(dA),
+                                                            sp), 5)
+    t_g = timed(torch, s, lambda: lib.dq_prefill_gemm_mxfp4(ctypes.byref(dA), ctypes.byref(dW), dq.OUT_BF16,
+                                                            ctypes.c_void_p(Y.data_ptr()), sp), 5)
+    flops = 2.0 * M * N * K
+    return {"quant_us": t_q * 1e6, "quant_GB/s": M * K * (2 + 0.5 + 1 / 32) / t_q / 1e9,
+            "gemm_us": t_g * 1e6, "gemm_TFLOP/s": flops / t_g / 1e12,
+            "frac_fp4_peak": flops / t_g / 1e12 / PEAK_FP4_TFLOPS,
+            "linear_TFLOP/s_incl_quant": flops / (t_q + t_g) / 1e12,
+            "note": "MXFP4 W4A4 (E2M1, E8M0 per 32 along K) on the scaled FP4 MFMA; same shapes, bf16 output"}
+
+
+def c2_fused(dq, synth, torch, np, lib, s, sp):
+    """27B MLP down-projection at an 8K prompt: M = 8192, K = 17408, N = 5120,
+    activation quantization fused into the prefill call (static scale, the
+    NVFP4 copy of X in a caller workspace)."""
+    cfg = synth.CONFIGS[2]
+    layer = cfg.layers[0]
+    M, N, K = cfg.m, layer.n, layer.k
+    W = dq.dq_pack_nvfp4(torch.from_numpy(synth.layer_weight(cfg, layer)).cuda())
+    X = torch.from_numpy(synth.prefill_x(cfg, K).view(np.int16)).cuda()
+    G = dq.dq_quantize_act_nvfp4(torch.from_numpy(synth.prefill_x(cfg, K, m=2048, calib=True).view(np.int16))
+                                 .cuda()).G.clone()
+    Y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    ws_n = dq.dq_prefill_gemm_workspace_size(M, K)
+    ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda")
+    dW = W.desc()
+    t = timed(torch, s, lambda: lib.dq_prefill_gemm(None, ctypes.c_void_p(X.data_ptr()), ctypes.c_void_p(G.data_ptr()),
+                                                    ctypes.byref(dW), M, dq.OUT_BF16, ctypes.c_void_p(Y.data_ptr()),
+                                                    None, None, 0, ctypes.c_void_p(ws.data_ptr()), ws_n, sp), 10)
+    flops = 2.0 * M * N * K
+    return {"us": t * 1e6, "TFLOP/s": flops / t / 1e12, "frac_fp4_peak": flops / t / 1e12 / PEAK_FP4_TFLOPS,
+            "frac_fp16_mfma_peak": flops / t / 1e12 / PEAK_FP16_TFLOPS,
+            "note": "one dq_prefill_gemm call with X: quantization pass into the workspace, then the GEMM"}
+
+
+def c3_chain(dq, synth, torch, np, lib, s, sp):
+    """The 27B block's linears chained on one stream at M = 4096: activation
+    quantization and q/k/v (bf16 out); quantization of the attention-output
+    stand-in and o with an NVFP4 epilogue (static scale) feeding gate/up with
+    SwiGLU and an NVFP4 epilogue feeding down (bf16 out)."""
+    cfg = synth.CONFIGS[3]
+    L = {l.name: l for l in cfg.layers}
+    M = cfg.m
+    W = {n: dq.dq_pack_nvfp4(torch.from_numpy(synth.layer_weight(cfg, L[n])).cuda()) for n in L}
+    X = torch.from_numpy(synth.prefill_x(cfg, 5120).view(np.int16)).cuda()
+    At = torch.from_numpy(synth.attn_out_standin(cfg, M, 5120).view(np.int16)).cuda()
+    g = lambda v: torch.tensor([v], dtype=torch.float32, device="cuda")   # noqa: E731
+    Gx = dq.dq_quantize_act_nvfp4(X[:2048]).G.clone()
+    Ga = dq.dq_quantize_act_nvfp4(At[:2048]).G.clone()
+    Go, Gh = g(0.02), g(0.05)
+    A1, A2 = dq.NvFp4Tensor.empty(M, 5120), dq.NvFp4Tensor.empty(M, 5120)
+    Ho = dq.NvFp4Tensor.empty(M, 5120)
+    Hg = dq.NvFp4Tensor.empty(M, 17408)
+    Yqkv = torch.empty((M, 7168), dtype=torch.bfloat16, device="cuda")
+    Yd = torch.empty((M, 5120), dtype=torch.bfloat16, device="cuda")
+    d = {k: v.desc() for k, v in W.items()}
+    dA1, dA2, dHo, dHg = A1.desc(), A2.desc(), Ho.desc(), Hg.desc()
+    P = ctypes.c_void_p
+    by = ctypes.byref
+
+    def chain():
+        assert lib.dq_quantize_act_nvfp4(P(X.data_ptr()), M, 5120, P(Gx.data_ptr()), by(dA1), sp) == 0
+        assert lib.dq_prefill_gemm(by(dA1), None, None, by(d["qkv"]), M, dq.OUT_BF16, P(Yqkv.data_ptr()), None, None,
+                                   0, None, 0, sp) == 0
+        assert lib.dq_quantize_act_nvfp4(P(At.data_ptr()), M, 5120, P(Ga.data_ptr()), by(dA2), sp) == 0
+        assert lib.dq_prefill_gemm(by(dA2), None, None, by(d["o"]), M, dq.OUT_NVFP4, None, P(Go.data_ptr()), by(dHo),
+                                   0, None, 0, sp) == 0
+        assert lib.dq_prefill_gemm(by(dHo), None, None, by(d["gate_up"]), M, dq.OUT_NVFP4, None, P(Gh.data_ptr()),
+                                   by(dHg), dq.EPI_SWIGLU, None, 0, sp) == 0
+        assert lib.dq_prefill_gemm(by(dHg), None, None, by(d["down"]), M, dq.OUT_BF16, P(Yd.data_ptr()), None, None,
+                                   0, None, 0, sp) == 0
+    t = timed(torch, s, chain, 10)
+    flops = 2.0 * M * sum(l.n * l.k for l in cfg.layers)
+    return {"us": t * 1e6, "TFLOP/s": flops / t / 1e12, "frac_fp4_peak": flops / t / 1e12 / PEAK_FP4_TFLOPS,
+            "frac_fp16_mfma_peak": flops / t / 1e12 / PEAK_FP16_TFLOPS, "TFLOP": flops / 1e12,
+            "note": "2 activation quantizations + 4 GEMMs (q/k/v bf16, o -> NVFP4, gate/up + SwiGLU -> NVFP4, "
+                    "down bf16), back-to-back on one stream"}
+
+
+def nvfp4a16_decode(dq, torch, lib, s, sp, Wq, N, K):
+    """Weight-only NVFP4 decode GEMV (format-disaggregated NVFP4) on the 27B
+    down-projection's NVFP4 weights, rotated over 16 copies (800 MB) so that
+    they stream from HBM."""
+    copies = [Wq] + [dq.NvFp4Tensor(Wq.codes.clone(), Wq.scales.clone(), Wq.G.clone(), N, K) for _ in range(15)]
+    ds = [c.desc() for c in copies]
+    nbytes = Wq.codes.numel() + Wq.scales.numel()
+    out = {}
+    for B in (1, 16):
+        x = torch.randn(B, K, device="cuda").to(torch.bfloat16)
+        y = torch.empty((B, N), dtype=torch.float32, device="cuda")
+        ws_n = dq.dq_decode_gemv_nvfp4_workspace_size(B, Wq)
+        ws = torch.empty(max(ws_n, 16), dtype=torch.uint8, device="cuda")
+        it = iter(range(1 << 30))
+        t = timed(torch, s, lambda: lib.dq_decode_gemv_nvfp4(ctypes.c_void_p(x.data_ptr()), B,
+                                                             ctypes.byref(ds[next(it) % len(ds)]), dq.OUT_F32,
+                                                             ctypes.c_void_p(y.data_ptr()),
+                                                             ctypes.c_void_p(ws.data_ptr()), ws_n, sp), 32)
+        alg = nbytes + B * K * 2 + B * N * 4
+        out[f"b{B}"] = {"us": t * 1e6, "GB/s": alg / t / 1e9, "frac_hbm": alg / t / 1e9 / PEAK_HBM_GBS}
+    out["note"] = "NVFP4 weights (4.5 bits/weight), bf16 x; back-to-back calls over 16 weight copies"
+    return out
 
 
 if __name__ == "__main__":

@@ -10,10 +10,13 @@
  * Conventions for every call
  *   - Buffers are device memory owned by the caller.  The library keeps no
  *     state except a thread-local last-error string and a per-device memory
- *     pool, from which it takes stream-ordered staging only for
- *     dq_prefill_gemm's fused path, dq_autocast_lut_to_nvfp4, and the
- *     calls that take a workspace (the GEMVs, the fused RMSNorm quantizer)
- *     when they are given none.
+ *     pool.  Calls that need scratch memory take a caller workspace (with a
+ *     size query): dq_prefill_gemm's fused path, dq_decode_gemv,
+ *     dq_decode_gemv_nvfp4 and dq_rmsnorm_quantize_act_nvfp4.  Given a
+ *     workspace they allocate nothing; given NULL they take stream-ordered
+ *     staging from the pool (hipMallocFromPoolAsync / hipFreeAsync on the
+ *     call's stream).  dq_autocast_lut_to_nvfp4 (an offline, load-time step)
+ *     always takes its fp32 staging from the pool.  No other call allocates.
  *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*;
  *     NULL is the default stream).  Nothing synchronizes inside the library.
  *   - Arguments are validated on the host before any HIP call; a rejected
@@ -36,7 +39,7 @@
 extern "C" {
 #endif
 
-#define DQ_ABI_VERSION 2
+#define DQ_ABI_VERSION 3
 
 typedef int32_t dq_status;
 #define DQ_OK 0
@@ -203,17 +206,21 @@ dq_status dq_quantize_act_nvfp4(const uint16_t* X, int64_t M, int64_t K, const f
                                 const dq_nvfp4_t* out, void* stream);
 
 /* ---- a3 (+a1 fused, +a4): W4A4 NVFP4 GEMM --------------------------------
- * Y[m, n] = G_a * G_w * sum_k a[m, k] * w[n, k] over the dequantized NVFP4
- * operands (exact products, fp32 accumulation).
+ * The prefill projection of the W4A4 NVFP4 format (App. A "Quantization
+ * formats", NVFP4: activations quantized with a static per-tensor input
+ * scale; App. C "Prefill measurements", compute and timing scope: the
+ * quantized projections with their activation processing fused):
+ *   Y[m, n] = G_a * G_w * sum_k a[m, k] * w[n, k]
+ * over the dequantized NVFP4 operands (exact products, fp32 accumulation).
  * A: quantized activations (rows = M, cols = K) - or NULL together with
  *   X (device bf16 [M, K]) and G_x_static (device float): the activations are
  *   then quantized with the static scale as part of this call (fused a1), by
- *   one streaming pass into NVFP4 staging that the GEMM reads.  The staging
- *   (M x K / 2 + M x K / 16 bytes, tile-rounded) is taken with
- *   hipMallocAsync and released with hipFreeAsync on `stream`, so concurrent
- *   calls on different streams do not share it; this is the only call that
- *   allocates.  Exactly one of A and X must be given (with M == 0 the fused
- *   call may pass X = NULL).
+ *   one streaming pass into an NVFP4 copy that the GEMM reads.  That copy
+ *   lives in `workspace` (at least dq_prefill_gemm_workspace_size(M, K)
+ *   bytes, 16-byte aligned, not in use by other work while the call runs on
+ *   `stream`); with workspace == NULL it is taken from the library's pool,
+ *   stream-ordered.  Exactly one of A and X must be given (with M == 0 the
+ *   fused call may pass X = NULL).  The unfused call ignores the workspace.
  * W: packed weights, rows = N, cols = K (same K as A).
  * out_kind DQ_OUT_F32 / DQ_OUT_BF16: Y is device [M, N] row-major fp32 / bf16
  *   (bf16: round to nearest even).
@@ -224,10 +231,11 @@ dq_status dq_quantize_act_nvfp4(const uint16_t* X, int64_t M, int64_t K, const f
  *   16 (rows 32j..32j+15 = gate rows 16j.., rows 32j+16..32j+31 = up rows
  *   16j..); the output column j = silu(gate_j) * up_j, N/2 columns.
  * K % 16 == 0, M >= 0, N >= 0. */
+dq_status dq_prefill_gemm_workspace_size(int64_t M, int64_t K, size_t* bytes);
 dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G_x_static,
                           const dq_nvfp4_t* W, int64_t M, int out_kind, void* Y,
                           const float* G_out_static, const dq_nvfp4_t* Yq, int epilogue_flags,
-                          void* stream);
+                          void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---- RMSNorm fused with the NVFP4 activation quantizer -------------------
  * The paper quantizes activations inside the normalization that feeds the
@@ -308,11 +316,12 @@ dq_status dq_prefill_gemm_mxfp4(const dq_mxfp4_t* A, const dq_mxfp4_t* W, int ou
  * Activations are converted to fp16 inside the kernel after a power-of-two
  * rescale from the largest magnitude of the slice of x that one wavefront
  * (B = 1) or one K group of a batch row (B >= 2) reads; a bf16 value is
- * converted exactly unless it lies more than 2^24 below that magnitude (it
- * then rounds as an fp16 subnormal).  Products with the fp16 table are
- * exact; partial sums are scaled back by the same power of two.  In
- * PAPER_GRID mode the block scale is folded into the fp16 operand (one
- * rounding, relative 2^-11 per weight). */
+ * converted exactly unless it lies more than 2^31 below that magnitude (it
+ * then becomes an fp16 subnormal, truncated toward zero: an error below 2^-38
+ * of the magnitude).  Products with the fp16 table are exact; partial sums
+ * are scaled back by the same power of two.  In PAPER_GRID mode the product
+ * grid[code] * e4m3(scale) (up to 15 significant bits) is rounded once to an
+ * fp16 operand: each weight carries a relative error of at most 2^-11. */
 dq_status dq_decode_gemv_workspace_size(int64_t B, const dq_lut_t* W, size_t* bytes);
 dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y,
                          void* workspace, size_t workspace_bytes, void* stream);

@@ -65,8 +65,9 @@ def _load() -> ctypes.CDLL:
         "dq_pack_nvfp4": (S, [P, I64, I64, P, ctypes.POINTER(_NvFp4), P]),
         "dq_pack_lut3": (S, [P, I64, I64, I32, I32, P, ctypes.POINTER(_Lut), P]),
         "dq_quantize_act_nvfp4": (S, [P, I64, I64, P, ctypes.POINTER(_NvFp4), P]),
+        "dq_prefill_gemm_workspace_size": (S, [I64, I64, SZ]),
         "dq_prefill_gemm": (S, [ctypes.POINTER(_NvFp4), P, P, ctypes.POINTER(_NvFp4), I64, I32, P, P,
-                                ctypes.POINTER(_NvFp4), I32, P]),
+                                ctypes.POINTER(_NvFp4), I32, P, ctypes.c_size_t, P]),
         "dq_autocast_lut_to_nvfp4": (S, [ctypes.POINTER(_Lut), P, ctypes.POINTER(_NvFp4), P]),
         "dq_rmsnorm_quantize_act_nvfp4": (S, [P, P, ctypes.c_float, I64, I64, P, ctypes.POINTER(_NvFp4), P,
                                               ctypes.c_size_t, P]),
@@ -89,6 +90,7 @@ def _load() -> ctypes.CDLL:
 _lib = _load()
 EXPORTED = ("dq_abi_version", "dq_status_string", "dq_last_error", "dq_nvfp4_sizes", "dq_lut_sizes",
             "dq_pack_nvfp4", "dq_pack_lut3", "dq_quantize_act_nvfp4", "dq_prefill_gemm",
+            "dq_prefill_gemm_workspace_size",
             "dq_decode_gemv_workspace_size", "dq_decode_gemv", "dq_mxfp4_sizes", "dq_pack_mxfp4",
             "dq_quantize_act_mxfp4", "dq_prefill_gemm_mxfp4", "dq_decode_gemv_nvfp4_workspace_size",
             "dq_decode_gemv_nvfp4", "dq_autocast_lut_to_nvfp4", "dq_rmsnorm_quantize_act_nvfp4")
@@ -255,11 +257,25 @@ def dq_quantize_act_nvfp4(X: torch.Tensor, G_static: Optional[torch.Tensor] = No
     return out
 
 
+def dq_prefill_gemm_workspace_size(M: int, K: int) -> int:
+    """Workspace bytes of dq_prefill_gemm's fused path (X given) for an [M, K] activation."""
+    out = ctypes.c_size_t()
+    _check(_lib.dq_prefill_gemm_workspace_size(M, K, ctypes.byref(out)), "dq_prefill_gemm_workspace_size")
+    return out.value
+
+
 def dq_prefill_gemm(W: NvFp4Tensor, A: Optional[NvFp4Tensor] = None, X: Optional[torch.Tensor] = None,
                     G_x_static: Optional[torch.Tensor] = None, out_kind: int = OUT_F32,
                     Y: Optional[torch.Tensor] = None, G_out_static: Optional[torch.Tensor] = None,
-                    Yq: Optional[NvFp4Tensor] = None, epilogue_flags: int = 0, stream=None):
+                    Yq: Optional[NvFp4Tensor] = None, epilogue_flags: int = 0, stream=None,
+                    workspace: Optional[torch.Tensor] = None):
     M = A.rows if A is not None else X.shape[0]
+    if X is not None and workspace is None:
+        # the NVFP4 copy of X, from torch's stream-ordered caching allocator
+        workspace = torch.empty(max(dq_prefill_gemm_workspace_size(M, W.cols), 16), dtype=torch.uint8,
+                                device=W.codes.device)
+    ws_ptr, ws_bytes = (workspace.data_ptr(), workspace.numel() * workspace.element_size()) \
+        if workspace is not None else (None, 0)
     n_out = W.rows // 2 if (epilogue_flags & EPI_SWIGLU) else W.rows
     dev = W.codes.device
     if out_kind == OUT_NVFP4:
@@ -272,7 +288,8 @@ def dq_prefill_gemm(W: NvFp4Tensor, A: Optional[NvFp4Tensor] = None, X: Optional
     xp = _as_u16(X).data_ptr() if X is not None else None
     _check(_lib.dq_prefill_gemm(ctypes.byref(da) if da is not None else None, xp, _ptr(G_x_static),
                                 ctypes.byref(dw), M, out_kind, _ptr(Y), _ptr(G_out_static),
-                                ctypes.byref(dyq) if dyq is not None else None, epilogue_flags, _stream(stream)),
+                                ctypes.byref(dyq) if dyq is not None else None, epilogue_flags, ws_ptr, ws_bytes,
+                                _stream(stream)),
            "dq_prefill_gemm")
     return Yq if out_kind == OUT_NVFP4 else Y
 

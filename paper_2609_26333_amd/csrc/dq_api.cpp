@@ -279,9 +279,23 @@ dq_status dq_quantize_act_nvfp4(const uint16_t* X, int64_t M, int64_t K, const f
                     "dq_quantize_act_nvfp4");
 }
 
+// Bytes of the NVFP4 copy of X that the fused path of dq_prefill_gemm stages:
+// codes and scales in the tiled layout, plus 16 bytes for its global scale.
+static size_t fused_staging_bytes(int64_t M, int64_t K) {
+  const int64_t r = rup(M, 32), c = rup(K, 64);
+  return (size_t)(r * c / 2) + (size_t)(r * c / 16) + 16;
+}
+
+dq_status dq_prefill_gemm_workspace_size(int64_t M, int64_t K, size_t* bytes) {
+  if (bytes == nullptr) return fail(DQ_ERR_INVALID_ARG, "bytes is NULL");
+  if (M < 0 || K < 0 || K % 16 != 0) return fail(DQ_ERR_INVALID_ARG, "M >= 0, K >= 0, K %% 16 == 0 required");
+  *bytes = fused_staging_bytes(M, K);
+  return ok();
+}
+
 dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G_x_static, const dq_nvfp4_t* W,
                           int64_t M, int out_kind, void* Y, const float* G_out_static, const dq_nvfp4_t* Yq,
-                          int epilogue_flags, void* stream) {
+                          int epilogue_flags, void* workspace, size_t workspace_bytes, void* stream) {
   // exactly one of A and X; an empty fused call (M == 0) may pass X = NULL
   if (A != nullptr && X != nullptr) return fail(DQ_ERR_INVALID_ARG, "give exactly one of A and X");
   if (A == nullptr && X == nullptr && !(M == 0 && G_x_static != nullptr))
@@ -299,6 +313,8 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
     if (G_x_static == nullptr || !aligned(G_x_static, 4))
       return fail(DQ_ERR_INVALID_ARG, "the fused path needs an aligned G_x_static");
     if (!aligned(X, 16)) return fail(DQ_ERR_INVALID_ARG, "X must be 16-byte aligned");
+    if (workspace != nullptr && (!aligned(workspace, 16) || workspace_bytes < fused_staging_bytes(M, K)))
+      return fail(DQ_ERR_INVALID_ARG, "workspace must be 16-byte aligned and hold dq_prefill_gemm_workspace_size() bytes");
   }
   if (epilogue_flags & ~DQ_EPI_SWIGLU) return fail(DQ_ERR_INVALID_ARG, "unknown epilogue flag");
   const bool swiglu = (epilogue_flags & DQ_EPI_SWIGLU) != 0;
@@ -321,23 +337,26 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
   }
   dq::GemmArgs a{};
   hipStream_t hs = (hipStream_t)stream;
-  void* staging = nullptr;
+  void* staging = nullptr;   // pooled staging to release after the GEMM
   if (A) {
     a.A = view(A);
   } else {
-    // Fused activation quantization: one streaming pass of X into NVFP4
-    // staging (stream-ordered allocation), then the GEMM, then the release,
-    // all on `stream`.
+    // Fused activation quantization: one streaming pass of X into the NVFP4
+    // copy in the workspace (or in stream-ordered pool staging), then the
+    // GEMM, all on `stream`.
     const int64_t r = rup(M, 32), c = rup(K, 64);
     const size_t code_bytes = (size_t)(r * c / 2), scale_bytes = (size_t)(r * c / 16);
-    const size_t bytes = code_bytes + scale_bytes + 16;
-    hipError_t e = dq::pool_alloc_async(&staging, bytes, hs);
-    if (e != hipSuccess) return hip_status(e, "dq_prefill_gemm (staging)");
-    uint8_t* base = static_cast<uint8_t*>(staging);
+    void* base_ptr = workspace;
+    if (base_ptr == nullptr) {
+      hipError_t e = dq::pool_alloc_async(&staging, fused_staging_bytes(M, K), hs);
+      if (e != hipSuccess) return hip_status(e, "dq_prefill_gemm (staging)");
+      base_ptr = staging;
+    }
+    uint8_t* base = static_cast<uint8_t*>(base_ptr);
     a.A = dq::NvFp4View{base, base + code_bytes, reinterpret_cast<float*>(base + code_bytes + scale_bytes), M, K};
-    e = dq::launch_quantize_act(X, M, K, G_x_static, a.A, hs);
+    hipError_t e = dq::launch_quantize_act(X, M, K, G_x_static, a.A, hs);
     if (e != hipSuccess) {
-      (void)hipFreeAsync(staging, hs);
+      if (staging != nullptr) (void)hipFreeAsync(staging, hs);
       return hip_status(e, "dq_prefill_gemm (activation quantization)");
     }
   }

@@ -29,6 +29,11 @@ hipError_t launch_quantize_act(const uint16_t* X, int64_t M, int64_t K, const fl
 hipError_t launch_pack_nvfp4(const float* W, int64_t N, int64_t K, const float* G_override,
                              const NvFp4View& out, hipStream_t s);
 
+// G = fp32(max|x| / 2688) of n fp32 values into *G (1 when all are zero):
+// the global scale of the NVFP4 weight rule, shared by the paper-grid LUT
+// packer (quant.hip)
+hipError_t launch_global_scale_f32(const float* x, int64_t n, float* G, hipStream_t s);
+
 // a5: LUT packing (pack_lut.hip)
 hipError_t launch_pack_lut(const float* W, int64_t N, int64_t K, const uint16_t* grid_host,
                            const LutView& out, hipStream_t s);

@@ -530,9 +530,6 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
     split = 0;
   else if (rounds > 0 && rest > 0 && 4 * rest <= slots)
     split = rounds * slots / tm * Gm::bn;
-#if defined(DQ_GEMM_GEO) && DQ_GEMM_GEO == 1
-  split = a.N;
-#endif
   return launch_geo<Gm, Gh>(a, split, s);
 }
 

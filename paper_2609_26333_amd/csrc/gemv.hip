@@ -349,7 +349,7 @@ __device__ inline void reduce_store(float4_t acc, float4_t* red, int wave, int l
 // Each activation chunk is consumed by exactly one wavefront, which stages it
 // itself: it loads its own raw bf16 chunks straight into LDS, rescales them by
 // a power of two taken from their own maximum (so the fp16 copy is exact for
-// every value within 2^40 of that maximum) and converts them in place; its
+// every value within 2^31 of that maximum) and converts them in place; its
 // partial sums are unscaled before the reduction.  Each wavefront also copies
 // the tables of its rounds into a private LDS slot.  Nothing is shared before
 // the reduction, so wavefronts start streaming without a barrier; the code
@@ -415,7 +415,7 @@ void lut_gemv_persist_kernel(const uint16_t* __restrict__ x, int B, int64_t K, c
     const i32x4_t rx = buffer_resource(x, (uint32_t)(K * 2));
 #pragma unroll
     for (int u = 0; u < (XREG > 0 ? XREG : 1); ++u)
-      xr[u] = (uint32_t)raw_buffer_load_b32(rx, lane * 4, ((u * W + wave) * 128) * 2, 0);
+      xr[u] = (uint32_t)raw_buffer_load_b32(rx, lane * 4 + ((u * W + wave) * 128) * 2, 0, 0);
   } else {
     for (int jj = 0; jj < B; ++jj)
       for (int c = wave; c < KCi; c += W) {
@@ -433,7 +433,7 @@ void lut_gemv_persist_kernel(const uint16_t* __restrict__ x, int B, int64_t K, c
 #pragma unroll
     for (int ti = 0; ti < TI; ++ti)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (__attribute__((address_space(3))) void*)(tabs + ti * 1024), 16,
-                                               lane * 16, t0 * kTabBytes + ti * 1024, 0, 0);
+                                               lane * 16 + t0 * kTabBytes + ti * 1024, 0, 0, 0);
   }
   uint4_t grid_tab{0u, 0u, 0u, 0u};
   if (MODE == 1) grid_tab = load_table<BITS>(lut);
@@ -482,15 +482,18 @@ void lut_gemv_persist_kernel(const uint16_t* __restrict__ x, int B, int64_t K, c
   }
   __builtin_amdgcn_sched_barrier(0);
   float unscale = 1.0f;
-  // the scaled values are exact in fp16, so the conversion's rounding mode
-  // is immaterial
+  // the scaled values are exact in fp16 down to 2^-17 (at most 2^32 below the
+  // maximum, which lands in [2^14, 2^15)); smaller ones become fp16 subnormals,
+  // truncated toward zero by the conversion (an error below 2^-24, i.e. 2^-38
+  // of the maximum)
   auto to_h2 = [](uint32_t v, float sc) {
     return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(bf16_lo(v) * sc, bf16_hi(v) * sc));
   };
   if constexpr (xreg) {
     float m = 0.0f;
 #pragma unroll
-    for (int u = 0; u < (XREG > 0 ? XREG : 1); ++u) m = fmaxf(m, fmaxf(fabsf(bf16_lo(xr[u])), fabsf(bf16_hi(xr[u]))));
+    for (int u = 0; u < (XREG > 0 ? XREG : 1); ++u)
+      if (u < nxc) m = fmaxf(m, fmaxf(fabsf(bf16_lo(xr[u])), fabsf(bf16_hi(xr[u]))));
     const int e = stage_exponent(__float_as_uint(wave_max_dpp(m)));
     const float sc = __builtin_ldexpf(1.0f, e);
     unscale = __builtin_ldexpf(1.0f, -e);
@@ -646,7 +649,7 @@ constexpr int kRingMulti = 8;
 // W * TPW row tiles.  It copies the bf16 slice of x (all B rows) into LDS,
 // one wavefront per batch row rescales the row's slice by a power of two
 // from the slice's own maximum and converts it to fp16 in place (exact for
-// every value within 2^40 of that maximum), and each wavefront then owns TPW
+// every value within 2^31 of that maximum), and each wavefront then owns TPW
 // whole tiles over the K group: its code stream is contiguous per tile and
 // it reduces nothing with other wavefronts.  The tile sums are unscaled per
 // batch row.  With one K group they are y; otherwise they go to a per-K-group
@@ -703,7 +706,7 @@ void lut_gemv_split_kernel(const uint16_t* __restrict__ x, int64_t K, int B, con
 #pragma unroll
     for (int ti = 0; ti < TI; ++ti)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (__attribute__((address_space(3))) void*)(tabs + ti * 1024), 16,
-                                               lane * 16, tw * kTabBytes + ti * 1024, 0, 0);
+                                               lane * 16 + tw * kTabBytes + ti * 1024, 0, 0, 0);
   }
   // the grid into LDS as well: with only the ring's loads tracked by the
   // compiler, its waits in the loop stay exact
@@ -1045,8 +1048,10 @@ __global__ __launch_bounds__(768) void lut_gemv_multi_kernel(const uint16_t* __r
   reduce_store(acc, red, wave, lane, ks, KS, tile_ok, tile, N, out_kind, y, xlane);
 }
 
-__global__ void zero_fill_kernel(uint32_t* p, int64_t n) {
-  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < n; t += (int64_t)gridDim.x * blockDim.x) p[t] = 0u;
+// n zero elements of 4 (fp32) or 2 (bf16) bytes
+template <typename T>
+__global__ void zero_fill_kernel(T* p, int64_t n) {
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < n; t += (int64_t)gridDim.x * blockDim.x) p[t] = 0;
 }
 
 constexpr int64_t kLdsPerCu = 160 * 1024;
@@ -1068,12 +1073,12 @@ inline int persist_wgs_per_cu(int vgprs, int waves, int64_t lds) {
 
 // Wavefront tasks per compute unit for the batched kernel.  Fewer tasks mean
 // fewer K groups: less partial-sum traffic and less activation staging per
-// weight byte.  Measured over the 27B and 8B decode linears at batch 2-16:
-// 12 is 0-13 % faster than 24 (all but the 27B down-projection at batch 16,
-// 7 % slower), 16 / 32 / 48 in between or slower.
-#ifndef DQ_GEMV_TASKS_PER_CU
-#define DQ_GEMV_TASKS_PER_CU 12
-#endif
+// weight byte, but fewer wavefronts streaming.  Measured over the 27B block
+// (q/k/v, o, gate/up, down), one call each in a captured graph: at batch 8,
+// 12 tasks 5 % faster than 6 in total (gate/up and down gain, the small
+// matrices lose); at batch 16, 6 tasks 12 % faster than 12 (the activation
+// staging of a K group grows with the batch); 24 and 48 slower everywhere.
+inline int64_t gemv_tasks_per_cu(int64_t B) { return B >= 12 ? 6 : 12; }
 
 // Plan of the batch B >= 2 split-K kernel (see lut_gemv_split_kernel).
 struct BatchedPlan {
@@ -1088,9 +1093,9 @@ inline BatchedPlan plan_batched(int bits, int64_t B, int64_t T, int64_t KC) {
   const int64_t tab_bytes = 32 << bits;
   BatchedPlan p{};
   p.ok = T * KC * 64 * (bits == 3 ? 12 : 8) < ((int64_t)1 << 31);
-  // wavefront tasks (one tile over one K group): DQ_GEMV_TASKS_PER_CU per
-  // compute unit; a K group's slice of x stays within ~40 KiB of LDS
-  const int64_t tasks = (int64_t)num_cus() * DQ_GEMV_TASKS_PER_CU;
+  // wavefront tasks (one tile over one K group) per compute unit; a K
+  // group's slice of x stays within ~40 KiB of LDS
+  const int64_t tasks = (int64_t)num_cus() * gemv_tasks_per_cu(B);
   const int64_t kcr_lds = std::max<int64_t>(1, (40 * 1024) / (B * 256));
   int64_t KG = std::max<int64_t>((KC + kcr_lds - 1) / kcr_lds, std::min<int64_t>(KC, (tasks + T - 1) / T));
   p.KCR = (KC + KG - 1) / KG;
@@ -1272,9 +1277,12 @@ hipError_t launch_gemv(const uint16_t* x, int64_t B, const LutView& w, int out_k
                        hipStream_t s) {
   if (w.rows == 0 || B == 0) return hipSuccess;
   if (w.cols == 0) {   // empty sum: y = 0 (fp32 or bf16 zeros are all-zero bits)
-    const int64_t words = (B * w.rows * (out_kind == 0 ? 4 : 2) + 3) / 4;
-    hipLaunchKernelGGL(zero_fill_kernel, dim3((unsigned)std::min<int64_t>(1024, (words + 255) / 256)), dim3(256), 0, s,
-                       reinterpret_cast<uint32_t*>(y), words);
+    const int64_t n = B * w.rows;
+    const dim3 grid((unsigned)std::min<int64_t>(1024, (n + 255) / 256));
+    if (out_kind == 0)
+      hipLaunchKernelGGL(zero_fill_kernel<uint32_t>, grid, dim3(256), 0, s, reinterpret_cast<uint32_t*>(y), n);
+    else
+      hipLaunchKernelGGL(zero_fill_kernel<uint16_t>, grid, dim3(256), 0, s, reinterpret_cast<uint16_t*>(y), n);
     return hipGetLastError();
   }
   if (w.bits == 3)

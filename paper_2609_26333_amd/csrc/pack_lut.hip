@@ -258,23 +258,6 @@ __global__ __launch_bounds__(256) void pack_lut_paper_kernel(const float* __rest
   sp[1] = (uint8_t)sb[1];
 }
 
-__global__ void zero_f32_one(float* p) { *p = 0.0f; }
-__global__ void finalize_g(float* p) {
-  const float a = *p;
-  *p = (a == 0.0f) ? 1.0f : a / kGlobalDivisor;
-}
-__global__ __launch_bounds__(256) void amax_f32_kernel(const float* __restrict__ x, int64_t n, float* out) {
-  float m = 0.0f;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-    m = fmaxf(m, fabsf(x[i]));
-  __shared__ float part[4];
-  m = wave_max(m);
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
-  __syncthreads();
-  if (threadIdx.x == 0) atomic_max_nonneg(out, fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3])));
-}
-
-
 // ---------------------------------------------------------------- autocast
 // LUT -> NVFP4 autocast, step 1: the dequantized LUT weight as fp32 [N, K],
 // one thread per 32-code group of the tiled layout (dq.h).  PER_ROW entries
@@ -361,12 +344,8 @@ hipError_t launch_pack_lut(const float* W, int64_t N, int64_t K, const uint16_t*
     g.v[i] = src[i];
     if ((src[i] & 0x7FFFu) == 0) zl = i;
   }
-  hipLaunchKernelGGL(zero_f32_one, dim3(1), dim3(1), 0, s, out.G);
-  int64_t nb = (N * K + 255) / 256;
-  if (nb > 1024) nb = 1024;
-  if (nb < 1) nb = 1;
-  hipLaunchKernelGGL(amax_f32_kernel, dim3((unsigned)nb), dim3(256), 0, s, W, N * K, out.G);
-  hipLaunchKernelGGL(finalize_g, dim3(1), dim3(1), 0, s, out.G);
+  hipError_t e = launch_global_scale_f32(W, N * K, out.G, s);   // G = max|W| / 2688, the NVFP4 rule
+  if (e != hipSuccess) return e;
   const int64_t threads = N16 * KC * 4;
   const int64_t blocks = (threads + 255) / 256;
   if (out.bits == 3)

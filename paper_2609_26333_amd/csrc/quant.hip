@@ -330,6 +330,10 @@ hipError_t launch_rmsnorm_quantize_act(const uint16_t* X, const uint16_t* gamma,
   return e;
 }
 
+hipError_t launch_global_scale_f32(const float* x, int64_t n, float* G, hipStream_t s) {
+  return launch_amax(x, n, G, s);
+}
+
 hipError_t launch_pack_nvfp4(const float* W, int64_t N, int64_t K, const float* G_override,
                              const NvFp4View& out, hipStream_t s) {
   if (G_override == nullptr) {

@@ -28,7 +28,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert dq.abi_version() == 2
+    assert dq.abi_version() == 3
     lib = dq.lib()
     assert lib.dq_status_string(0) == b"DQ_OK"
     assert lib.dq_status_string(-1) == b"DQ_ERR_INVALID_ARG"
@@ -51,6 +51,11 @@ def test_size_queries():
     assert dq.mxfp4_sizes(100, 96) == (128 * 128 // 2, 128 * 128 // 32)
     assert dq.mxfp4_sizes(130, 64) == (160 * 64 // 2, 256 * 64 // 32)
     assert dq.mxfp4_sizes(0, 0) == (0, 0)
+    # fused prefill staging: the NVFP4 copy of X (tile-rounded) plus its global scale
+    assert dq.dq_prefill_gemm_workspace_size(100, 48) == 128 * 64 // 2 + 128 * 64 // 16 + 16
+    assert dq.dq_prefill_gemm_workspace_size(0, 64) == 16
+    with pytest.raises(dq.DQError):
+        dq.dq_prefill_gemm_workspace_size(4, 24)
     with pytest.raises(dq.DQError):
         dq.mxfp4_sizes(4, 48)
 
@@ -98,45 +103,51 @@ def test_invalid_arguments_rejected_on_host():
     a = _nv(4, 32, fake, fake, fake)
     w = _nv(8, 32, fake, fake, fake)
     assert lib.dq_prefill_gemm(ctypes.byref(a), fake, fake, ctypes.byref(w), 4, 0, fake, None, None, 0,
-                               None) == dq.DQ_ERR_INVALID_ARG
+                               None, 0, None) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_prefill_gemm(None, None, None, ctypes.byref(w), 4, 0, fake, None, None, 0,
+                               None, 0, None) == dq.DQ_ERR_INVALID_ARG
+    # GEMM: fused path with a workspace that is too small or misaligned
+    need = dq.dq_prefill_gemm_workspace_size(4, 32)
+    assert lib.dq_prefill_gemm(None, fake, fake, ctypes.byref(w), 4, 0, fake, None, None, 0, fake, need - 1,
+                               None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_prefill_gemm(None, fake, fake, ctypes.byref(w), 4, 0, fake, None, None, 0, fake + 8, need,
                                None) == dq.DQ_ERR_INVALID_ARG
     # GEMM: K mismatch between A and W
     a2 = _nv(4, 48, fake, fake, fake)
     assert lib.dq_prefill_gemm(ctypes.byref(a2), None, None, ctypes.byref(w), 4, 0, fake, None, None, 0,
-                               None) == dq.DQ_ERR_INVALID_ARG
+                               None, 0, None) == dq.DQ_ERR_INVALID_ARG
     # GEMM: bad out kind, bad flag
     assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w), 4, 7, fake, None, None, 0,
-                               None) == dq.DQ_ERR_INVALID_ARG
+                               None, 0, None) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w), 4, 0, fake, None, None, 4,
-                               None) == dq.DQ_ERR_INVALID_ARG
+                               None, 0, None) == dq.DQ_ERR_INVALID_ARG
     # SwiGLU needs gate/up groups of 16 rows (W rows % 32 == 0)
     w48 = _nv(48, 32, fake, fake, fake)
     assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w48), 4, 0, fake, None, None,
-                               dq.EPI_SWIGLU, None) == dq.DQ_ERR_INVALID_ARG
+                               dq.EPI_SWIGLU, None, 0, None) == dq.DQ_ERR_INVALID_ARG
     # NVFP4 output: Y must be NULL, Yq and G_out given, Yq shaped [M, N] ([M, N/2] with SwiGLU)
     w64 = _nv(64, 32, fake, fake, fake)
     yq = _nv(4, 64, fake, fake, fake)
     yq_sw = _nv(4, 32, fake, fake, fake)
     assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w64), 4, dq.OUT_NVFP4, fake, fake,
-                               ctypes.byref(yq), 0, None) == dq.DQ_ERR_INVALID_ARG
+                               ctypes.byref(yq), 0, None, 0, None) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w64), 4, dq.OUT_NVFP4, None, None,
-                               ctypes.byref(yq), 0, None) == dq.DQ_ERR_INVALID_ARG
+                               ctypes.byref(yq), 0, None, 0, None) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w64), 4, dq.OUT_NVFP4, None, fake,
-                               None, 0, None) == dq.DQ_ERR_INVALID_ARG
+                               None, 0, None, 0, None) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w64), 4, dq.OUT_NVFP4, None, fake,
-                               ctypes.byref(yq_sw), 0, None) == dq.DQ_ERR_INVALID_ARG
+                               ctypes.byref(yq_sw), 0, None, 0, None) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w64), 4, dq.OUT_NVFP4, None, fake,
-                               ctypes.byref(yq), dq.EPI_SWIGLU, None) == dq.DQ_ERR_INVALID_ARG
+                               ctypes.byref(yq), dq.EPI_SWIGLU, None, 0, None) == dq.DQ_ERR_INVALID_ARG
     # Yq with a plain output
     assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w64), 4, 0, fake, None,
-                               ctypes.byref(yq), 0, None) == dq.DQ_ERR_INVALID_ARG
+                               ctypes.byref(yq), 0, None, 0, None) == dq.DQ_ERR_INVALID_ARG
     # NVFP4 output columns must be a multiple of 16 (here 40 / 2 = 20 after SwiGLU is refused first;
     # 24 rows without SwiGLU)
     w24 = _nv(24, 32, fake, fake, fake)
     yq24 = _nv(4, 24, fake, fake, fake)
     assert lib.dq_prefill_gemm(ctypes.byref(a), None, None, ctypes.byref(w24), 4, dq.OUT_NVFP4, None, fake,
-                               ctypes.byref(yq24), 0, None) == dq.DQ_ERR_INVALID_ARG
+                               ctypes.byref(yq24), 0, None, 0, None) == dq.DQ_ERR_INVALID_ARG
     # GEMV: batch out of range, bad bits
     lw = dq._Lut(fake, fake, None, None, 16, 128, 3, 0)
     assert lib.dq_decode_gemv(fake, 0, ctypes.byref(lw), 0, fake, None, 0, None) == dq.DQ_ERR_INVALID_ARG

@@ -14,6 +14,7 @@ import torch
 
 sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
 import dq_layout as L  # noqa: E402
+import parity_bounds as PB  # noqa: E402
 
 import synth  # noqa: E402
 from oracle import formats, linalg, mxfp4  # noqa: E402
@@ -133,8 +134,11 @@ def test_mx_gemm_oracle_operands(M, N, K):
     err = linalg.rel_fro(y, ref)
     say("  rel_fro", err)
     assert err <= TOL
+    bound = PB.fp32_sum_bound(PB.abs_products(mxfp4.dequantize(qa, sa), mxfp4.dequantize(qw, sw)), K)
+    PB.assert_within(y, ref, bound, "mx gemm f32")
     yb = host(dq.dq_prefill_gemm_mxfp4(A, W, out_kind=dq.OUT_BF16).float()).astype(np.float64)
     assert linalg.rel_fro(yb, formats.bf16_rne_from_f64(ref)) <= TOL
+    PB.assert_within(yb, ref, bound, "mx gemm bf16", bf16=True)
 
 
 def test_mx_gemm_exact_small_scales():
@@ -173,6 +177,8 @@ def test_mx_gemm_end_to_end_c1_sampled_rows():
     err = linalg.rel_fro(y, formats.bf16_rne_from_f64(ref))
     say("  c1 sampled rel_fro", err)
     assert err <= TOL
+    bound = PB.fp32_sum_bound(PB.abs_products(mxfp4.dequantize(qa, sa), mxfp4.dequantize(qw, sw)), layer.k)
+    PB.assert_within(y, ref, bound, "mx c1 gemm", bf16=True)
 
 
 @pytest.mark.parametrize("M,N,K", [(0, 64, 64), (64, 0, 64), (40, 24, 0)])

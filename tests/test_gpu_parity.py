@@ -2,7 +2,8 @@
 
 Bars: codes, scales, LUT entries and global scales bit-exact; GEMM / GEMV
 fp32 outputs within 1e-3 relative Frobenius error of the fp64 oracle (bf16
-outputs against the oracle rounded to bf16).  Inputs are seeded synthetic
+outputs against the oracle rounded to bf16) and, element by element, within
+the fp32 summation bound of parity_bounds.py.  Inputs are seeded synthetic
 tensors (synth/); no expected value comes from the GPU.
 """
 import ctypes
@@ -15,6 +16,7 @@ import torch
 
 sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
 import dq_layout as L  # noqa: E402
+import parity_bounds as PB  # noqa: E402
 
 import synth  # noqa: E402
 from oracle import formats, linalg, lut, nvfp4  # noqa: E402
@@ -166,9 +168,12 @@ def test_gemm_oracle_operands(M, N, K):
     err = linalg.rel_fro(y, ref)
     say("  rel_fro", err)
     assert err <= TOL
+    bound = PB.fp32_sum_bound(PB.abs_products(nvfp4.dequantize(qa, ca, Ga), nvfp4.dequantize(qw, cw, Gw)), K)
+    PB.assert_within(y, ref, bound, "gemm f32")
     yb = dq.dq_prefill_gemm(W, A=A, out_kind=dq.OUT_BF16)
     ybf = host(yb.float()).astype(np.float64)
     assert linalg.rel_fro(ybf, formats.bf16_rne_from_f64(ref)) <= TOL
+    PB.assert_within(ybf, ref, bound, "gemm bf16", bf16=True)
 
 
 def test_gemm_exact_unit_scales():
@@ -208,6 +213,8 @@ def test_gemm_end_to_end_c1_sampled_rows():
     err = linalg.rel_fro(y, formats.bf16_rne_from_f64(ref))
     say("  c1 sampled rel_fro", err)
     assert err <= TOL
+    bound = PB.fp32_sum_bound(PB.abs_products(nvfp4.dequantize(qa, ca, G_x), nvfp4.dequantize(qw, cw, Gw)), layer.k)
+    PB.assert_within(y, ref, bound, "c1 gemm", bf16=True)
 
 
 @pytest.mark.parametrize("M,N,K,out", [(2048, 10240, 256, "bf16"), (1024, 20480, 128, "nvfp4"),
@@ -313,6 +320,8 @@ def test_gemm_fused_c2_full_size_sampled():
     err = linalg.rel_fro(y, formats.bf16_rne_from_f64(ref))
     say("  c2 fused sampled rel_fro", err)
     assert err <= TOL
+    bound = PB.fp32_sum_bound(PB.abs_products(nvfp4.dequantize(qa, ca, G_x), nvfp4.dequantize(qw, cw, Gw)), layer.k)
+    PB.assert_within(y, ref, bound, "c2 fused gemm", bf16=True)
 
 
 def test_gemm_empty():
@@ -329,7 +338,8 @@ def _lut_weight(N, K, seed):
 
 
 LUT_CASES = [(512, 512, 1, 3), (20, 96, 1, 3), (20, 96, 3, 2), (48, 4096, 4, 2), (12288, 4096, 1, 3),
-             (12288, 4096, 4, 3), (64, 4096, 16, 3), (40, 17408, 16, 3), (5120, 17408, 1, 3)]
+             (12288, 4096, 4, 3), (12288, 4096, 1, 2), (12288, 4096, 4, 2), (64, 4096, 16, 3), (40, 17408, 16, 3),
+             (5120, 17408, 1, 3), (33, 640, 1, 2), (33, 640, 2, 3)]
 
 
 @pytest.mark.parametrize("N,K,B,bits", LUT_CASES)
@@ -348,6 +358,8 @@ def test_lut_per_row_pack_and_gemv(N, K, B, bits):
     err = linalg.rel_fro(y, ref)
     say("  gemv rel_fro", err)
     assert err <= TOL
+    PB.assert_within(y, ref, PB.gemv_bound(formats.f64_from_bf16_bits(xb), lut.dequantize_per_row(codes_ref, lut_ref), K),
+                     "lut per-row gemv")
     if K <= 4096:
         yb = host(dq.dq_decode_gemv(bf16_dev(xb), Wq, out_kind=dq.OUT_BF16).float()).astype(np.float64)
         assert linalg.rel_fro(yb, formats.bf16_rne_from_f64(ref)) <= TOL
@@ -373,6 +385,8 @@ def test_lut_paper_grid_pack_and_gemv(N, K, B, bits):
     err = linalg.rel_fro(y, ref)
     say("  gemv rel_fro", err)
     assert err <= TOL
+    w_hat = lut.dequantize_paper_grid(codes_ref, sb_ref, G_ref, grid)
+    PB.assert_within(y, ref, PB.gemv_bound(formats.f64_from_bf16_bits(xb), w_hat, K, 2.0 ** -11), "lut paper gemv")
 
 
 def test_lut_paper_grid_custom_grid():
@@ -449,6 +463,8 @@ def test_nvfp4a16_gemv(N, K, B):
     err = linalg.rel_fro(y, ref)
     say("  rel_fro", err)
     assert err <= TOL
+    PB.assert_within(y, ref, PB.gemv_bound(formats.f64_from_bf16_bits(xb), nvfp4.dequantize(qw, cw, Gw), K),
+                     "nvfp4a16 gemv")
     if K <= 5120:
         yb = host(dq.dq_decode_gemv_nvfp4(bf16_dev(xb), Wq, out_kind=dq.OUT_BF16).float()).astype(np.float64)
         assert linalg.rel_fro(yb, formats.bf16_rne_from_f64(ref)) <= TOL

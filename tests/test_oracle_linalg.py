@@ -140,3 +140,26 @@ def test_silu_mul_values():
 def test_rel_fro():
     assert linalg.rel_fro(np.array([1.0, 2.0]), np.array([1.0, 2.0])) == 0.0
     assert abs(linalg.rel_fro(np.array([3.0, 4.0]) * 1.001, np.array([3.0, 4.0])) - 1e-3) < 1e-12
+
+
+def test_elementwise_bound_holds_for_fp32_sums_and_catches_a_wrong_element():
+    """The element-wise bound the GPU parity tests apply (tests/parity_bounds.py):
+    an fp32 GEMM of exactly representable dequantized operands (NumPy float32
+    matmul, any summation order) stays within it, and a single wrong output
+    (one flipped code's worth) does not."""
+    import parity_bounds as PB
+    rng = np.random.default_rng(5)
+    qa = rng.integers(0, 16, (24, 2048)).astype(np.uint8)
+    qw = rng.integers(0, 16, (40, 2048)).astype(np.uint8)
+    ca = rng.integers(0x30, 0x48, (24, 128)).astype(np.uint8)
+    cw = rng.integers(0x30, 0x48, (40, 128)).astype(np.uint8)
+    a_hat = nvfp4.dequantize(qa, ca, np.float32(0.01))
+    w_hat = nvfp4.dequantize(qw, cw, np.float32(0.02))
+    ref = linalg.gemm(a_hat, w_hat)
+    y32 = np.matmul(a_hat.astype(np.float32), w_hat.astype(np.float32).T).astype(np.float64)
+    bound = PB.fp32_sum_bound(PB.abs_products(a_hat, w_hat), 2048)
+    PB.assert_within(y32, ref, bound, "fp32 matmul")
+    bad = y32.copy()
+    bad[3, 7] += 0.5 * abs(a_hat[3]).max() * abs(w_hat[7]).max()   # one product's worth of error
+    with pytest.raises(AssertionError):
+        PB.assert_within(bad, ref, bound, "perturbed")
