@@ -326,6 +326,22 @@ dq_status dq_decode_gemv_workspace_size(int64_t B, const dq_lut_t* W, size_t* by
 dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y,
                          void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---- a6 without allocation -----------------------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid it): dq_decode_gemv
+ * with its split-K partial sums in a static scratch array of the library
+ * (DQ_NOALLOC_SCRATCH_BYTES per GPU, held by each GPU the library runs on
+ * until the process ends) instead of a workspace.  Same arguments, kernels
+ * and results as dq_decode_gemv; it calls no allocator.  A call whose partial
+ * sums exceed the scratch (dq_decode_gemv_workspace_size() above
+ * DQ_NOALLOC_SCRATCH_BYTES) is rejected with DQ_ERR_UNSUPPORTED before any
+ * GPU work.  Every call on one GPU shares that GPU's scratch: calls that
+ * overlap in time on one GPU (different streams, or different threads
+ * without ordering) race and give undefined results. */
+#define DQ_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+dq_status dq_decode_gemv_noalloc(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y,
+                                 void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -79,6 +79,7 @@ def _load() -> ctypes.CDLL:
         "dq_prefill_gemm_mxfp4": (S, [ctypes.POINTER(_MxFp4), ctypes.POINTER(_MxFp4), I32, P, P]),
         "dq_decode_gemv_workspace_size": (S, [I64, ctypes.POINTER(_Lut), SZ]),
         "dq_decode_gemv": (S, [P, I64, ctypes.POINTER(_Lut), I32, P, P, ctypes.c_size_t, P]),
+        "dq_decode_gemv_noalloc": (S, [P, I64, ctypes.POINTER(_Lut), I32, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -93,7 +94,8 @@ EXPORTED = ("dq_abi_version", "dq_status_string", "dq_last_error", "dq_nvfp4_siz
             "dq_prefill_gemm_workspace_size",
             "dq_decode_gemv_workspace_size", "dq_decode_gemv", "dq_mxfp4_sizes", "dq_pack_mxfp4",
             "dq_quantize_act_mxfp4", "dq_prefill_gemm_mxfp4", "dq_decode_gemv_nvfp4_workspace_size",
-            "dq_decode_gemv_nvfp4", "dq_autocast_lut_to_nvfp4", "dq_rmsnorm_quantize_act_nvfp4")
+            "dq_decode_gemv_nvfp4", "dq_autocast_lut_to_nvfp4", "dq_rmsnorm_quantize_act_nvfp4",
+            "dq_decode_gemv_noalloc")
 
 
 def lib() -> ctypes.CDLL:
@@ -418,5 +420,25 @@ def dq_decode_gemv(x: torch.Tensor, W: LutWeight, out_kind: int = OUT_F32, y: Op
     return y
 
 
+NOALLOC_SCRATCH_BYTES = 16 << 20
+
+
+def dq_decode_gemv_noalloc(x: torch.Tensor, W: LutWeight, out_kind: int = OUT_F32,
+                           y: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """dq_decode_gemv without a workspace: split-K partial sums go to the
+    library's static per-GPU scratch (calls overlapping on one GPU race)."""
+    x = _as_u16(x)
+    assert x.is_contiguous() and x.dim() == 2
+    B = x.shape[0]
+    if y is None:
+        y = torch.empty((B, W.rows), dtype=torch.float32 if out_kind == OUT_F32 else torch.bfloat16,
+                        device=x.device)
+    d = W.desc()
+    _check(_lib.dq_decode_gemv_noalloc(x.data_ptr(), B, ctypes.byref(d), out_kind, y.data_ptr(), _stream(stream)),
+           "dq_decode_gemv_noalloc")
+    return y
+
+
 __all__ = [n for n in dir() if n.startswith(("dq_", "DQ", "OUT_", "LUT_", "EPI_")) or n in
-           ("NvFp4Tensor", "MxFp4Tensor", "LutWeight", "nvfp4_sizes", "mxfp4_sizes", "lut_sizes", "abi_version", "lib", "EXPORTED")]
+           ("NvFp4Tensor", "MxFp4Tensor", "LutWeight", "nvfp4_sizes", "mxfp4_sizes", "lut_sizes", "abi_version", "lib", "EXPORTED",
+            "NOALLOC_SCRATCH_BYTES")]

@@ -458,8 +458,7 @@ dq_status dq_decode_gemv_workspace_size(int64_t B, const dq_lut_t* W, size_t* by
   return DQ_OK;
 }
 
-dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y, void* workspace,
-                         size_t workspace_bytes, void* stream) {
+static dq_status check_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y) {
   dq_status st = check_lut(W, "W");
   if (st != DQ_OK) return st;
   if (B < 1 || B > 16) return fail(DQ_ERR_INVALID_ARG, "1 <= B <= 16 required");
@@ -468,6 +467,28 @@ dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int ou
   if (out_kind != DQ_OUT_F32 && out_kind != DQ_OUT_BF16) return fail(DQ_ERR_INVALID_ARG, "bad out_kind");
   if (y == nullptr && W->rows > 0) return fail(DQ_ERR_INVALID_ARG, "y is NULL");
   if (!aligned(y, 16)) return fail(DQ_ERR_INVALID_ARG, "y must be 16-byte aligned");
+  return DQ_OK;
+}
+
+dq_status dq_decode_gemv_noalloc(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y,
+                                 void* stream) {
+  dq_status st = check_gemv(x, B, W, out_kind, y);
+  if (st != DQ_OK) return st;
+  const size_t need = dq::gemv_workspace_bytes(B, view(W));
+  if (need > dq::gemv_noalloc_scratch_bytes())
+    return fail(DQ_ERR_UNSUPPORTED, "dq_decode_gemv_noalloc: this call needs %zu bytes of scratch, the library's "
+                "static scratch holds %zu; use dq_decode_gemv with a workspace", need,
+                dq::gemv_noalloc_scratch_bytes());
+  void* ws = nullptr;
+  hipError_t e = dq::gemv_noalloc_scratch(&ws);
+  if (e != hipSuccess) return hip_status(e, "dq_decode_gemv_noalloc (scratch address)");
+  return hip_status(dq::launch_gemv(x, B, view(W), out_kind, y, ws, (hipStream_t)stream), "dq_decode_gemv_noalloc");
+}
+
+dq_status dq_decode_gemv(const uint16_t* x, int64_t B, const dq_lut_t* W, int out_kind, void* y, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  dq_status st = check_gemv(x, B, W, out_kind, y);
+  if (st != DQ_OK) return st;
   if (workspace != nullptr) {
     if (!aligned(workspace, 16)) return fail(DQ_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
     if (workspace_bytes < dq::gemv_workspace_bytes(B, view(W)))

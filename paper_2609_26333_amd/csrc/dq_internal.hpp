@@ -124,6 +124,10 @@ hipError_t launch_gemv_nvfp4(const uint16_t* x, int64_t B, const NvFp4View& w, i
 // a6: LUT GEMV (gemv.hip).  ws: workspace of at least
 // gemv_workspace_bytes(B, w) bytes, or NULL to take it from the pool.
 size_t gemv_workspace_bytes(int64_t B, const LutView& w);
+// The no-allocation variant's per-device static scratch (gemv.hip): its size,
+// and its device address on the current device (looked up on first use).
+size_t gemv_noalloc_scratch_bytes();
+hipError_t gemv_noalloc_scratch(void** ptr);
 hipError_t launch_gemv(const uint16_t* x, int64_t B, const LutView& w, int out_kind, void* y, void* ws,
                        hipStream_t s);
 

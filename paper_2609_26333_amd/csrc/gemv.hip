@@ -26,7 +26,9 @@
 #include <algorithm>
 #include <atomic>
 #include <cstdint>
+#include <mutex>
 
+#include "dq.h"
 #include "dq_device.hpp"
 #include "dq_internal.hpp"
 
@@ -1266,6 +1268,36 @@ pieces:
 }
 
 }  // namespace
+
+// Scratch of dq_decode_gemv_noalloc: the split-K partial sums of batch >= 2
+// calls, for callers that cannot allocate.  Each GPU the library runs on
+// holds its own copy until the process ends; its device address is looked up
+// once per device (host code must never pass the array's name itself: that
+// is a host-side stand-in).  Calls that overlap on one GPU share it and race.
+// The partial sums are written in full by the split kernel before the
+// reduction reads them, so nothing needs clearing between calls.
+constexpr size_t kNoallocScratchBytes = DQ_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kNoallocScratchBytes];
+
+size_t gemv_noalloc_scratch_bytes() { return kNoallocScratchBytes; }
+
+hipError_t gemv_noalloc_scratch(void** ptr) {
+  static std::mutex mu;
+  static void* dev_ptr[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (dev_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    dev_ptr[dev] = p;
+  }
+  *ptr = dev_ptr[dev];
+  return hipSuccess;
+}
 
 size_t gemv_workspace_bytes(int64_t B, const LutView& w) {
   if (B < 2 || w.rows == 0 || w.cols == 0) return 0;

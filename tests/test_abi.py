@@ -161,6 +161,14 @@ def test_invalid_arguments_rejected_on_host():
     assert lib.dq_decode_gemv_workspace_size(16, ctypes.byref(big), ctypes.byref(ws)) == dq.DQ_OK and ws.value > 0
     assert lib.dq_decode_gemv_workspace_size(17, ctypes.byref(big), ctypes.byref(ws)) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_decode_gemv(fake, 16, ctypes.byref(big), 0, fake, fake, ws.value - 16, None) == dq.DQ_ERR_INVALID_ARG
+    # the no-allocation GEMV: same argument checks; partial sums beyond its static scratch are refused
+    assert lib.dq_decode_gemv_noalloc(fake, 17, ctypes.byref(big), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
+    assert lib.dq_decode_gemv_noalloc(fake, 1, ctypes.byref(lw_bad), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
+    huge = dq._Lut(fake, fake, None, None, 131072, 5120, 3, 0)
+    assert lib.dq_decode_gemv_workspace_size(16, ctypes.byref(huge), ctypes.byref(ws)) == dq.DQ_OK
+    assert ws.value > dq.NOALLOC_SCRATCH_BYTES
+    assert lib.dq_decode_gemv_noalloc(fake, 16, ctypes.byref(huge), 0, fake, None) == dq.DQ_ERR_UNSUPPORTED
+    assert b"scratch" in lib.dq_last_error()
     # NVFP4A16 GEMV: batch range, K % 16, short workspace
     wn = _nv(7168, 5120, fake, fake, fake)
     assert lib.dq_decode_gemv_nvfp4(fake, 0, ctypes.byref(wn), 0, fake, None, 0, None) == dq.DQ_ERR_INVALID_ARG
