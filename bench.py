@@ -88,7 +88,57 @@ def parse():
     p.add_argument("--no-sclk", action="store_true")
     p.add_argument("--sweep-blocks", type=int, default=64)
     p.add_argument("--calibrate-copy", action="store_true")
+    p.add_argument("--summarize-trace", metavar="CSV", help="print a rocprofv3 kernel trace grouped by kernel and grid")
+    p.add_argument("--summarize-counters", metavar="CSV", help="print rocprofv3 counters grouped by kernel and grid")
     return p.parse_args()
+
+
+def short_kernel_name(name):
+    """Kernel name without namespaces, return type and argument list."""
+    n = name.strip('"')
+    n = re.sub(r"^void ", "", n)
+    n = n.replace("dq::(anonymous namespace)::", "").replace("dq::", "")
+    depth, cut = 0, len(n)
+    for i, ch in enumerate(n):        # the argument list: the first "(" outside template brackets
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            cut = i
+            break
+    return n[:cut].replace("(anonymous namespace)::", "")
+
+
+def summarize_trace(path, top=40):
+    """Markdown table of a rocprofv3 kernel trace: dispatches grouped by kernel,
+    grid and workgroup size, with calls and average / min / max duration."""
+    import csv
+    groups = {}
+    for r in csv.DictReader(open(path)):
+        key = (short_kernel_name(r["Kernel_Name"]), int(r["Grid_Size_X"]), int(r["Workgroup_Size_X"]))
+        groups.setdefault(key, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    rows = sorted(groups.items(), key=lambda kv: -sum(kv[1]))[:top]
+    print("| kernel | grid (work-items) | workgroup | calls | average (us) | min (us) | max (us) | total (us) |")
+    print("|---|---:|---:|---:|---:|---:|---:|---:|")
+    for (k, g, w), d in rows:
+        print(f"| `{k}` | {g} | {w} | {len(d)} | {sum(d) / len(d):.3f} | {min(d):.3f} | {max(d):.3f} | {sum(d):.1f} |")
+
+
+def summarize_counters(path):
+    """Markdown table of a rocprofv3 counter collection: the average value per
+    dispatch of each counter, grouped by kernel and grid size."""
+    import csv
+    groups = {}
+    for r in csv.DictReader(open(path)):
+        key = (short_kernel_name(r["Kernel_Name"]), int(r["Grid_Size"]), r["Counter_Name"])
+        groups.setdefault(key, {}).setdefault(int(r["Dispatch_Id"]), 0.0)
+        groups[key][int(r["Dispatch_Id"])] += float(r["Counter_Value"])
+    print("| kernel | grid (work-items) | counter | dispatches | average per dispatch |")
+    print("|---|---:|---|---:|---:|")
+    for (k, g, c), d in sorted(groups.items()):
+        v = list(d.values())
+        print(f"| `{k}` | {g} | {c} | {len(v)} | {sum(v) / len(v):.6g} |")
 
 
 def gemm_source_sha256():
@@ -199,6 +249,12 @@ def main():
         sys.exit(2)
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.summarize_trace or args.summarize_counters:
+        if args.summarize_trace:
+            summarize_trace(args.summarize_trace)
+        if args.summarize_counters:
+            summarize_counters(args.summarize_counters)
         return
     sampler = clk_path = None
     if not args.no_sclk:
