@@ -431,6 +431,7 @@ def run(args, clk_path):
         out["c2_fused_m8192"] = c2_fused(dq, synth, torch, np, lib, s, sp)
         out["c3_block_chain_m4096"] = c3_chain(dq, synth, torch, np, lib, s, sp)
         out["nvfp4a16_decode_27b_down"] = nvfp4a16_decode(dq, torch, lib, s, sp, Wq, N, K)
+        out["rmsnorm_quant_27b_hidden"] = rmsnorm_quant(dq, synth, torch, np, lib, s, sp)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w_down, X_host, np.float32(out["config"]["static_G_x"]))
     return out
@@ -561,6 +562,34 @@ def c3_chain(dq, synth, torch, np, lib, s, sp):
             "frac_fp16_mfma_peak": flops / t / 1e12 / PEAK_FP16_TFLOPS, "TFLOP": flops / 1e12,
             "note": "2 activation quantizations + 4 GEMMs (q/k/v bf16, o -> NVFP4, gate/up + SwiGLU -> NVFP4, "
                     "down bf16), back-to-back on one stream"}
+
+
+def rmsnorm_quant(dq, synth, torch, np, lib, s, sp):
+    """RMSNorm fused with the NVFP4 activation quantizer (static scale) on the
+    27B hidden state at M = 4096 and M = 32768, K = 5120, next to the plain
+    activation quantizer of the same tensor."""
+    cfg = synth.CONFIGS[3]
+    K = 5120
+    out = {}
+    X0 = torch.from_numpy(synth.prefill_x(cfg, K).view(np.int16)).cuda()
+    gamma = torch.from_numpy(synth.bf16_bits_from_f32((1.0 + 0.2 * synth.random_f32(7, (1, K))).astype(np.float32))[0]
+                             .view(np.int16)).cuda()
+    G = dq.dq_quantize_act_nvfp4(X0[:2048]).G.clone()
+    for M in (4096, 32768):
+        X = X0.repeat(M // X0.shape[0], 1)
+        A = dq.NvFp4Tensor.empty(M, K)
+        dA = A.desc()
+        P = ctypes.c_void_p
+        t_n = timed(torch, s, lambda: lib.dq_rmsnorm_quantize_act_nvfp4(P(X.data_ptr()), P(gamma.data_ptr()),
+                                                                         ctypes.c_float(1e-6), M, K, P(G.data_ptr()),
+                                                                         ctypes.byref(dA), None, 0, sp), 20)
+        t_q = timed(torch, s, lambda: lib.dq_quantize_act_nvfp4(P(X.data_ptr()), M, K, P(G.data_ptr()),
+                                                                ctypes.byref(dA), sp), 20)
+        nbytes = M * K * (2 + 0.5 + 1 / 16)
+        out[f"m{M}"] = {"rmsnorm_quant_us": t_n * 1e6, "rmsnorm_quant_GB/s": nbytes / t_n / 1e9,
+                        "quant_us": t_q * 1e6, "quant_GB/s": nbytes / t_q / 1e9}
+    out["note"] = "one pass over X (static scale, K <= 8192); algorithmic bytes: X read once, NVFP4 written"
+    return out
 
 
 def nvfp4a16_decode(dq, torch, lib, s, sp, Wq, N, K):

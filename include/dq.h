@@ -244,9 +244,11 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
  * inv = fp32(1 / fp32(sqrt(fp32(ms + eps)))), y = fp32(fp32(x * inv) * gamma)
  * with gamma device bf16 [K] (16-byte aligned); y is then quantized by the
  * a1 rule of dq_quantize_act_nvfp4 (G_static, or G = amax(y) / 2688 when
- * NULL).  out: rows = M, cols = K.  workspace: device memory of at least
- * 4 M bytes (16-byte aligned) for the per-row statistics, not in use by
- * other work during the call; NULL takes it from the library's pool,
+ * NULL).  out: rows = M, cols = K.  With a static scale and K <= 8192 the
+ * call is one pass over X (each row normalized and quantized from registers)
+ * and uses no workspace; otherwise the per-row statistics go to `workspace`:
+ * device memory of at least 4 M bytes (16-byte aligned), not in use by other
+ * work during the call; NULL takes it from the library's pool,
  * stream-ordered.  eps must be finite, >= 0. */
 dq_status dq_rmsnorm_quantize_act_nvfp4(const uint16_t* X, const uint16_t* gamma, float eps, int64_t M,
                                         int64_t K, const float* G_static, const dq_nvfp4_t* out,

@@ -683,13 +683,13 @@ void lut_gemv_split_kernel(const uint16_t* __restrict__ x, int64_t K, int B, con
   const int ntw = max(0, min(TPW, T - tw));                 // and its tile count
   const int c0 = kg * KCR, nc = min(KCR, KC - c0);         // the K group's chunks
   const int rowstride = nc * 128 + 8;                       // fp16 per staged batch row (pad staggers banks)
-  // LDS: activations [B][rowstride] | tables [W][TI KiB] | tile sums [W][TPW][B][16] fp32;
-  // static: unscale factors and grid, copied by wavefront 0
+  // LDS: activations [B][rowstride] | tables [W][TI KiB]; static: unscale
+  // factors and grid, copied by wavefront 0.  Tile sums go straight from the
+  // accumulators to y or to the K group's partials, so LDS holds only what
+  // the streaming reads and more workgroups fit on a compute unit.
   __shared__ __align__(16) uint32_t s_small[32];
   _Float16* xs = reinterpret_cast<_Float16*>(smem);
   uint8_t* tabs = smem + round_up((int64_t)B * rowstride * 2, 16) + (size_t)wave * TI * 1024;
-  float* outs = reinterpret_cast<float*>(smem + round_up((int64_t)B * rowstride * 2, 16) + (size_t)W * TI * 1024) +
-                (size_t)wave * TPW * B * 16;
   const int i = lane & 15, j = lane & 15, q = lane >> 4;
   const bool xlane = j < B;
 
@@ -838,7 +838,7 @@ void lut_gemv_split_kernel(const uint16_t* __restrict__ x, int64_t K, int B, con
         if (MODE == 1) af = scale_half8(af, st < 2 ? s_lo : s_hi);
         pacc[st] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf[st], pacc[st], 0, 0, 0);
       }
-      if (++u == nc) {   // end of tile ti_: its sums into this wavefront's LDS outputs
+      if (++u == nc) {   // end of tile ti_: lane (q, j) stores rows 4q..4q+3 of batch row j
         u = 0;
         float4_t acc;
 #pragma unroll
@@ -846,7 +846,24 @@ void lut_gemv_split_kernel(const uint16_t* __restrict__ x, int64_t K, int B, con
           acc[r2] = ((pacc[0][r2] + pacc[1][r2]) + (pacc[2][r2] + pacc[3][r2])) * unscale;
 #pragma unroll
         for (int st = 0; st < 4; ++st) pacc[st] = float4_t{0.f, 0.f, 0.f, 0.f};
-        if (xlane) *reinterpret_cast<float4_t*>(outs + (ti_ * B + j) * 16 + 4 * q) = acc;
+        if (xlane) {
+          const int64_t tile = tw + ti_;
+          if (KG == 1) {
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) {
+              const int64_t row = tile * 16 + 4 * q + r2;
+              if (row < N) {
+                const int64_t o2 = (int64_t)j * N + row;
+                if (out_kind == 0)
+                  reinterpret_cast<float*>(y)[o2] = acc[r2];
+                else
+                  reinterpret_cast<uint16_t*>(y)[o2] = (uint16_t)f32_to_bf16_rne(acc[r2]);
+              }
+            }
+          } else {
+            *reinterpret_cast<float4_t*>(partials + (((int64_t)kg * T + tile) * B + j) * 16 + 4 * q) = acc;
+          }
+        }
         ++ti_;
         if (ti_ < ntw) table_pools<BITS>(tile_table(ti_), tl0, tl1, th0, th1);
       }
@@ -868,25 +885,6 @@ void lut_gemv_split_kernel(const uint16_t* __restrict__ x, int64_t K, int B, con
 #pragma unroll
   for (int r = 0; r < RING - 1; ++r)
     if (full + r < total) slot(r);
-  // ---- 4. store this wavefront's tile sums: y directly, or this K group's
-  // partials [KG][T][B][16]
-  const int nout = ntw * B * 16;
-  for (int e = lane; e < nout; e += 64) {
-    const int t = e / (16 * B), rem = e - t * 16 * B, jj = rem >> 4, row16 = rem & 15;
-    const int64_t row = (int64_t)(tw + t) * 16 + row16;
-    const float v = outs[e];
-    if (KG == 1) {
-      if (row < N) {
-        const int64_t o2 = (int64_t)jj * N + row;
-        if (out_kind == 0)
-          reinterpret_cast<float*>(y)[o2] = v;
-        else
-          reinterpret_cast<uint16_t*>(y)[o2] = (uint16_t)f32_to_bf16_rne(v);
-      }
-    } else {
-      partials[(((int64_t)kg * T + tw + t) * B + jj) * 16 + row16] = v;
-    }
-  }
 }
 
 // y[jj][row] = sum over the K groups, in order, of the split kernel's
@@ -1106,7 +1104,7 @@ inline BatchedPlan plan_batched(int bits, int64_t B, int64_t T, int64_t KC) {
   p.TI = (p.TPW * tab_bytes + 1023) / 1024;
   const int64_t TG = (T + kW * p.TPW - 1) / (kW * p.TPW);
   p.G = p.KG * TG;
-  p.lds = round_up(B * (p.KCR * 128 + 8) * 2, 16) + kW * p.TI * 1024 + kW * p.TPW * B * 16 * 4;
+  p.lds = round_up(B * (p.KCR * 128 + 8) * 2, 16) + kW * p.TI * 1024;
   p.partial_bytes = p.KG > 1 ? (size_t)(p.KG * T * B * 16 * 4) : 0;
   return p;
 }

@@ -247,6 +247,79 @@ __global__ __launch_bounds__(256) void rms_rows_kernel(const uint16_t* __restric
   }
 }
 
+// ------------------------------------------------------------ RMSNorm + quantization, one pass
+// For a static global scale and rows of at most 64 * 8 * NV elements (tile-
+// padded): one wavefront per row holds the row in registers (lane l: the
+// 8-element vectors v = l + 64 j), takes the sum of squares in fp64 in the
+// same order and tree as rms_rows_kernel (so `inv` is the same), normalizes,
+// and quantizes each 16-block (vectors v and v ^ 1 in lanes l and l ^ 1) into
+// the row's slots of the tiled layout: X is read once.  A workgroup of eight
+// wavefronts takes eight consecutive rows of one 32-row tile row, so the row
+// segments of each tile are written together.  Rows past M and columns past
+// K (tile padding) are written as zero codes and scales.
+template <int NV>
+__global__ __launch_bounds__(512) void rmsnorm_quantize_rows_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ gamma, float eps, int64_t M, int64_t K,
+    const float* __restrict__ Gp, uint8_t* __restrict__ codes, uint8_t* __restrict__ scales, int64_t tiles_c,
+    float* G_out) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 8 + (threadIdx.x >> 6);
+  const float G = *Gp;
+  if (blockIdx.x == 0 && threadIdx.x == 0 && G_out != nullptr) *G_out = G;
+  const int nvec = (int)(K / 8), nvec_pad = (int)(tiles_c * 8);
+  const bool live = row < M;   // uniform over the wavefront
+  uint4_t xr[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int v = lane + 64 * j;
+    xr[j] = uint4_t{0u, 0u, 0u, 0u};
+    if (live && v < nvec) xr[j] = *reinterpret_cast<const uint4_t*>(x + row * K + 8 * (int64_t)v);
+  }
+  float iv = 0.0f;
+  if (live) {
+    double ss = 0.0;
+#pragma unroll
+    for (int j = 0; j < NV; ++j)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const double a = bf16_lo(xr[j][t]), b = bf16_hi(xr[j][t]);
+        ss += a * a;
+        ss += b * b;
+      }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, 64);
+    const float ms = (float)(ss / (double)K);
+    const float r = ms + eps;
+    iv = 1.0f / sqrtf(r);
+  }
+  const int64_t tr = row / 32, rr = row % 32;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int v = lane + 64 * j;
+    if (64 * j >= nvec_pad) break;            // uniform: no vector of this j in the padded row
+    float f[8];
+    uint4_t gw{0u, 0u, 0u, 0u};
+    if (v < nvec) gw = *reinterpret_cast<const uint4_t*>(gamma + 8 * v);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {     // two roundings, in this order (zeros stay zero)
+      f[2 * t] = (bf16_lo(xr[j][t]) * iv) * bf16_lo(gw[t]);
+      f[2 * t + 1] = (bf16_hi(xr[j][t]) * iv) * bf16_hi(gw[t]);
+    }
+    uint32_t sc;
+    const uint32_t w = quantize8(f, G, sc);   // every lane takes part in the pair exchange
+    // the scales of the tile row's four 16-blocks, gathered in the lane with v % 8 == 0
+    const uint32_t s2 = (uint32_t)__shfl((int)sc, lane + 2, 64);
+    const uint32_t s4 = (uint32_t)__shfl((int)sc, lane + 4, 64);
+    const uint32_t s6 = (uint32_t)__shfl((int)sc, lane + 6, 64);
+    if (v < nvec_pad) {
+      const int64_t tile = tr * tiles_c + v / 8;
+      *reinterpret_cast<uint32_t*>(codes + tile * 1024 + rr * 32 + 4 * (v % 8)) = w;
+      if ((v & 7) == 0)
+        *reinterpret_cast<uint32_t*>(scales + tile * 128 + rr * 4) = sc | (s2 << 8) | (s4 << 16) | (s6 << 24);
+    }
+  }
+}
+
 // ------------------------------------------------------------ launchers
 static int grid_for(int64_t n_vec) {
   int64_t b = (n_vec + 255) / 256;
@@ -300,6 +373,22 @@ hipError_t launch_rmsnorm_quantize_act(const uint16_t* X, const uint16_t* gamma,
       return launch_quantize(X, M, K, out.G, out, s);
     }
     return launch_quantize(X, M, K, G_static, out, s);
+  }
+  if (G_static != nullptr && tiles_c * 8 <= 64 * 16) {
+    // one pass: the row lives in registers (at most 16 vectors of 8 per lane)
+    const int nv = (int)((tiles_c * 8 + 63) / 64);
+    typedef void (*kern_t)(const uint16_t*, const uint16_t*, float, int64_t, int64_t, const float*, uint8_t*,
+                           uint8_t*, int64_t, float*);
+    static const kern_t kerns[16] = {
+        rmsnorm_quantize_rows_kernel<1>,  rmsnorm_quantize_rows_kernel<2>,  rmsnorm_quantize_rows_kernel<3>,
+        rmsnorm_quantize_rows_kernel<4>,  rmsnorm_quantize_rows_kernel<5>,  rmsnorm_quantize_rows_kernel<6>,
+        rmsnorm_quantize_rows_kernel<7>,  rmsnorm_quantize_rows_kernel<8>,  rmsnorm_quantize_rows_kernel<9>,
+        rmsnorm_quantize_rows_kernel<10>, rmsnorm_quantize_rows_kernel<11>, rmsnorm_quantize_rows_kernel<12>,
+        rmsnorm_quantize_rows_kernel<13>, rmsnorm_quantize_rows_kernel<14>, rmsnorm_quantize_rows_kernel<15>,
+        rmsnorm_quantize_rows_kernel<16>};
+    hipLaunchKernelGGL(kerns[nv - 1], dim3((unsigned)(tiles_r * 4)), dim3(512), 0, s, X, gamma, eps, M, K, G_static,
+                       out.codes, out.scales, tiles_c, G_static == out.G ? nullptr : out.G);
+    return hipGetLastError();
   }
   float* inv = reinterpret_cast<float*>(ws);
   const bool pooled = inv == nullptr;
