@@ -371,6 +371,7 @@ def run(args, clk_path):
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
     ph = [sum(m[j].elapsed_time(m[j + 1]) for m in marks) / args.steps for j in range(n_ph)]   # ms
+    ph_med = [float(np.median([m[j].elapsed_time(m[j + 1]) for m in marks])) for j in range(n_ph)]   # ms
     t_quant, t_gemm = ph[0] * 1e-3, ph[1] * 1e-3
 
     flops = 2.0 * M * N * K
@@ -382,7 +383,8 @@ def run(args, clk_path):
     for j, (bits, B) in enumerate(SWEEP):
         t = ph[2 + j] * 1e-3
         gbs = (wbytes[bits] + io[B]) / t / 1e9
-        decode[f"lut{bits}_b{B}"] = {"ms_per_token": t * 1e3, "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
+        decode[f"lut{bits}_b{B}"] = {"ms_per_token": t * 1e3, "ms_per_token_median": ph_med[2 + j],
+                                     "GB/s": gbs, "frac_hbm": gbs / PEAK_HBM_GBS,
                                      "bytes": wbytes[bits] + io[B],
                                      "gemv_launches": args.sweep_blocks * len(cfg.layers)}
     gemm_alg_bytes = M * K * (0.5 + 1 / 16) + N * K * (0.5 + 1 / 16) + M * N * 2
@@ -397,7 +399,8 @@ def run(args, clk_path):
                                 "(K=17408, N=5120)"),
                    "M": M, "N": N, "K": K, "decode_batches": [1, 8, 16], "sweep_blocks": args.sweep_blocks,
                    "static_G_x": float(G_x.cpu()[0]), "decode_tokens": "captured HIP graphs, 256 GEMVs each"},
-        "prefill": {"quant_us": t_quant * 1e6, "quant_GB/s": quant_bytes / t_quant / 1e9,
+        "prefill": {"quant_us": t_quant * 1e6, "quant_us_median": ph_med[0] * 1e3,
+                    "gemm_us_median": ph_med[1] * 1e3, "quant_GB/s": quant_bytes / t_quant / 1e9,
                     "quant_frac_hbm": quant_bytes / t_quant / 1e9 / PEAK_HBM_GBS,
                     "gemm_us": t_gemm * 1e6, "gemm_TFLOP/s": gemm_tflops,
                     "frac_fp4_peak": gemm_tflops / PEAK_FP4_TFLOPS,
@@ -420,6 +423,8 @@ def run(args, clk_path):
                             "frac": decode["lut3_b1"]["frac_hbm"]},
     }
     if not args.no_extras:
+        out["decode_differencing"] = decode_differencing(dq, torch, lib, s, stacks[3], xs[1], ys[1], cfg,
+                                                         graphs[(3, 1)])
         del graphs, keep
         torch.cuda.synchronize()
         out["sclk"] = measure_clocks(dq, torch, lib, s, sp, gemm, stacks, xs, ys, cfg, clk_path)
@@ -435,6 +440,45 @@ def run(args, clk_path):
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w_down, X_host, np.float32(out["config"]["static_G_x"]))
     return out
+
+
+def decode_differencing(dq, torch, lib, s, stack, xs, ys, cfg, g_full):
+    """N-vs-2N differencing of the LUT3 batch-1 token: replays of a captured
+    graph over the first half of the blocks and of the full token's graph
+    (median of 7 timings of 5 replays each); the difference over the blocks
+    it adds is the per-block cost without the graph launch."""
+    half = len(stack) // 2
+    descs = [[w.desc() for w in blk] for blk in stack[:half]]
+    cap = torch.cuda.Stream()
+    g_half = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_half, stream=cap):
+        p = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        for d in descs:
+            for i in range(len(cfg.layers)):
+                assert lib.dq_decode_gemv(ctypes.c_void_p(xs[i].data_ptr()), 1, ctypes.byref(d[i]), dq.OUT_F32,
+                                          ctypes.c_void_p(ys[i].data_ptr()), None, 0, p) == 0
+    torch.cuda.synchronize()
+
+    def med(g):
+        g.replay()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(7):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            for _ in range(5):
+                g.replay()
+            e1.record(s)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) / 5)
+        return sorted(ts)[len(ts) // 2]
+
+    t_half, t_full = med(g_half), med(g_full)
+    n_full = len(stack)
+    return {"blocks": [half, n_full], "ms_per_replay_median": [t_half, t_full],
+            "us_per_block_differenced": (t_full - t_half) / (n_full - half) * 1e3,
+            "us_per_block_full_replay": t_full / n_full * 1e3,
+            "note": "LUT3 batch 1; graph over the first half of the blocks vs the whole token"}
 
 
 def timed(torch, s, fn, reps):

@@ -345,8 +345,9 @@ __device__ inline void reduce_store(float4_t acc, float4_t* red, int wave, int l
 
 // ---------------------------------------------------------------- persistent
 // Resident workgroups that loop over row tiles (used whenever the staged
-// activations fit in LDS).  Workgroup g of G owns row tiles g, g + G, ...
-// ("rounds"); its W wavefronts split every tile's K: wavefront w consumes
+// activations fit in LDS).  Workgroup g owns the R consecutive row tiles
+// g*R .. g*R + R - 1 ("rounds"; the last workgroup may have fewer); its W
+// wavefronts split every tile's K: wavefront w consumes
 // chunks w, w + W, ... of the tile (CPW = ceil(KC / W) slots per round).
 // Each activation chunk is consumed by exactly one wavefront, which stages it
 // itself: it loads its own raw bf16 chunks straight into LDS, rescales them by
@@ -1078,6 +1079,8 @@ inline int persist_wgs_per_cu(int vgprs, int waves, int64_t lds) {
 // 12 tasks 5 % faster than 6 in total (gate/up and down gain, the small
 // matrices lose); at batch 16, 6 tasks 12 % faster than 12 (the activation
 // staging of a K group grows with the batch); 24 and 48 slower everywhere.
+// (Timed alone, 64 calls of one matrix in a row, q/k/v and o at batch 8 run
+// faster with 6 tasks; in the token's order of matrices they do not.)
 inline int64_t gemv_tasks_per_cu(int64_t B) { return B >= 12 ? 6 : 12; }
 
 // Plan of the batch B >= 2 split-K kernel (see lut_gemv_split_kernel).
