@@ -481,9 +481,18 @@ def decode_differencing(dq, torch, lib, s, stack, xs, ys, cfg, g_full):
             "note": "LUT3 batch 1; graph over the first half of the blocks vs the whole token"}
 
 
-def timed(torch, s, fn, reps):
+def timed(torch, s, fn, reps, warm_s=0.3):
+    """Mean time of `reps` back-to-back calls, after at least warm_s seconds of
+    back-to-back calls: the engine clock ramps up over tens of milliseconds
+    of sustained load (a few calls right after an idle gap run up to 20 %
+    slower), and the timed steps of the workload run in that sustained state."""
     fn()
     torch.cuda.synchronize()
+    t0 = time.time()
+    while time.time() - t0 < warm_s:
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(s)
     for _ in range(reps):
