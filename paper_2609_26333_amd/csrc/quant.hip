@@ -204,7 +204,9 @@ __global__ __launch_bounds__(256) void quantize_tiles_kernel(const T* __restrict
 
 // ------------------------------------------------------------ RMSNorm rows
 // One wavefront per row: ss = sum of the squares (each exact in fp64) in
-// fp64, ms = fp32(ss / K), inv = fp32(1 / fp32(sqrt(fp32(ms + eps))))
+// fp64 (lane l takes the 8-element vectors l, l + 64, ...; square t of a
+// vector's 4 pairs goes to partial sum t; the four partials are added
+// pairwise, then the lanes in a butterfly), ms = fp32(ss / K), inv = fp32(1 / fp32(sqrt(fp32(ms + eps))))
 // (correctly rounded square root and division).  With amax != nullptr also
 // the maximum |fp32(fp32(x * inv) * gamma)| of the row (dynamic global scale).
 __global__ __launch_bounds__(256) void rms_rows_kernel(const uint16_t* __restrict__ x,
@@ -214,16 +216,17 @@ __global__ __launch_bounds__(256) void rms_rows_kernel(const uint16_t* __restric
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;   // uniform over the wavefront
   const uint16_t* xr = x + row * K;
-  double ss = 0.0;
+  double s4[4] = {0.0, 0.0, 0.0, 0.0};
   for (int64_t k = lane * 8; k < K; k += 512) {   // K % 16 == 0
     const uint4_t w = *reinterpret_cast<const uint4_t*>(xr + k);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const double a = bf16_lo(w[j]), b = bf16_hi(w[j]);
-      ss += a * a;
-      ss += b * b;
+      s4[j] = __builtin_fma(a, a, s4[j]);   // a * a is exact: the same as a rounded add
+      s4[j] = __builtin_fma(b, b, s4[j]);
     }
   }
+  double ss = (s4[0] + s4[1]) + (s4[2] + s4[3]);
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, 64);
   const float ms = (float)(ss / (double)K);
@@ -251,7 +254,8 @@ __global__ __launch_bounds__(256) void rms_rows_kernel(const uint16_t* __restric
 // For a static global scale and rows of at most 64 * 8 * NV elements (tile-
 // padded): one wavefront per row holds the row in registers (lane l: the
 // 8-element vectors v = l + 64 j), takes the sum of squares in fp64 in the
-// same order and tree as rms_rows_kernel (so `inv` is the same), normalizes,
+// same order and tree as rms_rows_kernel (so `inv` is the same), normalizes
+// (gamma staged once per workgroup in LDS),
 // and quantizes each 16-block (vectors v and v ^ 1 in lanes l and l ^ 1) into
 // the row's slots of the tiled layout: X is read once.  A workgroup of eight
 // wavefronts takes eight consecutive rows of one 32-row tile row, so the row
@@ -275,31 +279,36 @@ __global__ __launch_bounds__(512) void rmsnorm_quantize_rows_kernel(
     xr[j] = uint4_t{0u, 0u, 0u, 0u};
     if (live && v < nvec) xr[j] = *reinterpret_cast<const uint4_t*>(x + row * K + 8 * (int64_t)v);
   }
+  // gamma (zero past K) into LDS once per workgroup: the eight rows share it
+  __shared__ uint4_t gsh[64 * 16];
+  for (int v = threadIdx.x; v < nvec_pad; v += 512)
+    gsh[v] = v < nvec ? *reinterpret_cast<const uint4_t*>(gamma + 8 * v) : uint4_t{0u, 0u, 0u, 0u};
   float iv = 0.0f;
   if (live) {
-    double ss = 0.0;
+    double s4[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
     for (int j = 0; j < NV; ++j)
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const double a = bf16_lo(xr[j][t]), b = bf16_hi(xr[j][t]);
-        ss += a * a;
-        ss += b * b;
+        s4[t] = __builtin_fma(a, a, s4[t]);   // a * a is exact: the same as a rounded add
+        s4[t] = __builtin_fma(b, b, s4[t]);
       }
+    double ss = (s4[0] + s4[1]) + (s4[2] + s4[3]);
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, 64);
     const float ms = (float)(ss / (double)K);
     const float r = ms + eps;
     iv = 1.0f / sqrtf(r);
   }
+  __syncthreads();
   const int64_t tr = row / 32, rr = row % 32;
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
     const int v = lane + 64 * j;
     if (64 * j >= nvec_pad) break;            // uniform: no vector of this j in the padded row
     float f[8];
-    uint4_t gw{0u, 0u, 0u, 0u};
-    if (v < nvec) gw = *reinterpret_cast<const uint4_t*>(gamma + 8 * v);
+    const uint4_t gw = v < nvec_pad ? gsh[v] : uint4_t{0u, 0u, 0u, 0u};
 #pragma unroll
     for (int t = 0; t < 4; ++t) {     // two roundings, in this order (zeros stay zero)
       f[2 * t] = (bf16_lo(xr[j][t]) * iv) * bf16_lo(gw[t]);
