@@ -238,7 +238,25 @@ def cpu_baseline(w_down, X, G_x, min_seconds=10.0):
                    f"dequantization + fp64 GEMV of one 27B down-projection ({N}x{K}) at batch 1, "
                    f"{t_dec / reps:.2f} s each = {dec_bytes * reps / t_dec / 1e9:.3f} GB/s; packing untimed"),
         "decode_gbps": dec_bytes * reps / t_dec / 1e9,
+        "host": host_info(threadpool_info()),
     }
+
+
+def host_info(pools):
+    """The host the oracle ran on: logical CPUs, the CPU model, and the BLAS /
+    OpenMP thread pools numpy uses."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_count": os.cpu_count(), "model": model,
+            "thread_pools": [{"api": i.get("user_api"), "library": i.get("internal_api"),
+                              "threads": i.get("num_threads")} for i in pools]}
 
 
 def main():
