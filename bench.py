@@ -585,10 +585,20 @@ def c2_fused(dq, synth, torch, np, lib, s, sp):
     t = timed(torch, s, lambda: lib.dq_prefill_gemm(None, ctypes.c_void_p(X.data_ptr()), ctypes.c_void_p(G.data_ptr()),
                                                     ctypes.byref(dW), M, dq.OUT_BF16, ctypes.c_void_p(Y.data_ptr()),
                                                     None, None, 0, ctypes.c_void_p(ws.data_ptr()), ws_n, sp), 10)
+    # the two halves of the fused call, each timed alone: the quantization
+    # pass bounds what folding it into the GEMM could save
+    A = dq.NvFp4Tensor.empty(M, K)
+    dA = A.desc()
+    t_q = timed(torch, s, lambda: lib.dq_quantize_act_nvfp4(ctypes.c_void_p(X.data_ptr()), M, K,
+                                                            ctypes.c_void_p(G.data_ptr()), ctypes.byref(dA), sp), 10)
+    t_g = timed(torch, s, lambda: lib.dq_prefill_gemm(ctypes.byref(dA), None, None, ctypes.byref(dW), M, dq.OUT_BF16,
+                                                      ctypes.c_void_p(Y.data_ptr()), None, None, 0, None, 0, sp), 10)
     flops = 2.0 * M * N * K
     return {"us": t * 1e6, "TFLOP/s": flops / t / 1e12, "frac_fp4_peak": flops / t / 1e12 / PEAK_FP4_TFLOPS,
             "frac_fp16_mfma_peak": flops / t / 1e12 / PEAK_FP16_TFLOPS,
-            "note": "one dq_prefill_gemm call with X: quantization pass into the workspace, then the GEMM"}
+            "quant_pass_us": t_q * 1e6, "gemm_alone_us": t_g * 1e6,
+            "note": "one dq_prefill_gemm call with X: quantization pass into the workspace, then the GEMM; "
+                    "quant_pass_us and gemm_alone_us time the two halves alone"}
 
 
 def c3_chain(dq, synth, torch, np, lib, s, sp):
