@@ -449,6 +449,11 @@ def run(args, clk_path):
         del stacks
         torch.cuda.empty_cache()
         out["mxfp4_prefill_m32768"] = mxfp4_prefill(dq, torch, lib, s, sp, w_down, X, M, N, K)
+        c1 = synth.CONFIGS[1]
+        up = c1.layers[0]
+        out["mxfp4_prefill_8b_up_m2048"] = mxfp4_prefill(dq, torch, lib, s, sp, synth.layer_weight(c1, up),
+                                                         dev(synth.prefill_x(c1, up.k).view(np.int16)), c1.m,
+                                                         up.n, up.k, reps=100)
         del A, Y, X
         torch.cuda.empty_cache()
         out["c2_fused_m8192"] = c2_fused(dq, synth, torch, np, lib, s, sp)
@@ -548,7 +553,7 @@ def measure_clocks(dq, torch, lib, s, sp, gemm, stacks, xs, ys, cfg, clk_path):
     return res
 
 
-def mxfp4_prefill(dq, torch, lib, s, sp, w, X, M, N, K):
+def mxfp4_prefill(dq, torch, lib, s, sp, w, X, M, N, K, reps=5):
     """The MXFP4 W4A4 variant of the same prefill linear (OCP MX: E8M0 scale
     per 32, block scales applied inside the FP4 MFMA)."""
     Wm = dq.dq_pack_mxfp4(torch.from_numpy(w).cuda())
@@ -556,9 +561,9 @@ def mxfp4_prefill(dq, torch, lib, s, sp, w, X, M, N, K):
     Y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
     dA, dW = A.desc(), Wm.desc()
     t_q = timed(torch, s, lambda: lib.dq_quantize_act_mxfp4(ctypes.c_void_p(X.data_ptr()), M, K, ctypes.byref(dA),
-                                                            sp), 5)
+                                                            sp), reps)
     t_g = timed(torch, s, lambda: lib.dq_prefill_gemm_mxfp4(ctypes.byref(dA), ctypes.byref(dW), dq.OUT_BF16,
-                                                            ctypes.c_void_p(Y.data_ptr()), sp), 5)
+                                                            ctypes.c_void_p(Y.data_ptr()), sp), reps)
     flops = 2.0 * M * N * K
     return {"quant_us": t_q * 1e6, "quant_GB/s": M * K * (2 + 0.5 + 1 / 32) / t_q / 1e9,
             "gemm_us": t_g * 1e6, "gemm_TFLOP/s": flops / t_g / 1e12,
