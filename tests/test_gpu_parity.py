@@ -339,7 +339,11 @@ def _lut_weight(N, K, seed):
 
 LUT_CASES = [(512, 512, 1, 3), (20, 96, 1, 3), (20, 96, 3, 2), (48, 4096, 4, 2), (12288, 4096, 1, 3),
              (12288, 4096, 4, 3), (12288, 4096, 1, 2), (12288, 4096, 4, 2), (64, 4096, 16, 3), (40, 17408, 16, 3),
-             (5120, 17408, 1, 3), (33, 640, 1, 2), (33, 640, 2, 3)]
+             (5120, 17408, 1, 3), (33, 640, 1, 2), (33, 640, 2, 3),
+             # K not a multiple of the 128-column chunk (a partial last chunk),
+             # odd chunk counts, and batches on either side of the split plan's
+             # task-count switch at 12
+             (100, 4128, 1, 3), (100, 4128, 8, 2), (4112, 1056, 1, 3), (256, 4096, 12, 3), (96, 2080, 5, 3)]
 
 
 @pytest.mark.parametrize("N,K,B,bits", LUT_CASES)
