@@ -694,14 +694,19 @@ void lut_gemv_split_kernel(const uint16_t* __restrict__ x, int64_t K, int B, con
   const int i = lane & 15, j = lane & 15, q = lane >> 4;
   const bool xlane = j < B;
 
-  // ---- 1. the K group's slice of the raw bf16 activations (chunk-rows
-  // spread over the wavefronts; reads past K are clamped in bounds and zeroed
-  // at conversion) and this wavefront's tables
-  for (int t = wave; t < B * nc; t += W) {
-    const int b = t / nc, u = t - b * nc;
-    const int64_t k = min((int64_t)(c0 + u) * 128 + 2 * lane, K - 2);
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(x + (int64_t)b * K + k),
-                                     reinterpret_cast<void*>(xs + b * rowstride + u * 128), 4, 0, 0);
+  // ---- 1. the K group's slice of the raw bf16 activations, four chunks of
+  // a row per 16-byte-per-lane copy (spread over the wavefronts; lanes past
+  // the slice row stay idle, reads past K are clamped in bounds and zeroed at
+  // conversion) and this wavefront's tables
+  {
+    const int nq = (nc + 3) / 4;
+    for (int t = wave; t < B * nq; t += W) {
+      const int b = t / nq, u = 4 * (t - b * nq);
+      const int64_t k = min((int64_t)(c0 + u) * 128 + 8 * lane, K - 8);   // K % 32 == 0
+      if (lane < (nc - u) * 16)
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(x + (int64_t)b * K + k),
+                                         reinterpret_cast<void*>(xs + b * rowstride + u * 128), 16, 0, 0);
+    }
   }
   if (MODE == 0) {   // tables of tiles tw .. tw + TPW - 1 (contiguous); reads past the array return zero
     const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
@@ -760,26 +765,50 @@ void lut_gemv_split_kernel(const uint16_t* __restrict__ x, int64_t K, int B, con
   }
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_sched_barrier(0);
-  // ---- 2b. one wavefront per batch row: the slice's maximum, then fp16 in
-  // place; the row's unscale factor into LDS
+  // ---- 2b. per batch row, the slice's maximum, then fp16 in place; the
+  // row's unscale factor into LDS.  A row takes one wavefront (B <= W) or
+  // half of one (B > W: rows wave and wave + W side by side), its lanes
+  // striding over the row's dwords with eight reads in flight per round trip
   auto to_h2 = [](uint32_t v, float sc) {
     return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(bf16_lo(v) * sc, bf16_hi(v) * sc));
   };
-  for (int b = wave; b < B; b += W) {
-    uint32_t* row = reinterpret_cast<uint32_t*>(xs + b * rowstride);
+  {
+    const bool half = B > W;
+    const int tpr = half ? 32 : 64;                        // lanes per row
+    const int lr = half ? (lane & 31) : lane;
+    const int b = wave + (half ? W * (lane >> 5) : 0);
+    const bool live = b < B;                                // rows past B: reads only, of row 0
+    uint32_t* row = reinterpret_cast<uint32_t*>(xs + (live ? b : 0) * rowstride);
     const int nd = nc * 64;   // dwords of the slice row
     float m = 0.0f;
-    for (int d = lane; d < nd; d += 64) {
-      const uint32_t v = row[d];
-      m = fmaxf(m, fmaxf(fabsf(bf16_lo(v)), fabsf(bf16_hi(v))));
+    for (int d0 = lr; d0 < nd; d0 += 8 * tpr) {
+      uint32_t v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = d0 + u * tpr < nd ? row[d0 + u * tpr] : 0u;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) m = fmaxf(m, fmaxf(fabsf(bf16_lo(v[u])), fabsf(bf16_hi(v[u]))));
     }
-    const int e = stage_exponent(__float_as_uint(wave_max_dpp(m)));
+    m = fmaxf(m, __shfl_xor(m, 1, 64));
+    m = fmaxf(m, __shfl_xor(m, 2, 64));
+    m = fmaxf(m, __shfl_xor(m, 4, 64));
+    m = fmaxf(m, __shfl_xor(m, 8, 64));
+    m = fmaxf(m, __shfl_xor(m, 16, 64));
+    if (!half) m = fmaxf(m, __shfl_xor(m, 32, 64));
+    const int e = stage_exponent(__float_as_uint(m));
     const float sc = __builtin_ldexpf(1.0f, e);
-    for (int d = lane; d < nd; d += 64) {
-      const bool in_k = (int64_t)c0 * 128 + 2 * d < K;
-      row[d] = in_k ? to_h2(row[d], sc) : 0u;
+    if (live) {
+      for (int d0 = lr; d0 < nd; d0 += 8 * tpr) {
+        uint32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = d0 + u * tpr < nd ? row[d0 + u * tpr] : 0u;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int d = d0 + u * tpr;
+          if (d < nd) row[d] = (int64_t)c0 * 128 + 2 * d < K ? to_h2(v[u], sc) : 0u;
+        }
+      }
+      if (lr == 0) s_small[b] = __float_as_uint(__builtin_ldexpf(1.0f, -e));
     }
-    if (lane == 0) s_small[b] = __float_as_uint(__builtin_ldexpf(1.0f, -e));
   }
   __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
   __builtin_amdgcn_s_barrier();
