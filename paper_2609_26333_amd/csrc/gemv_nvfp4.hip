@@ -63,6 +63,13 @@ __device__ inline int nv_stage_exponent(uint32_t mb) {
 constexpr int kNvWaves = 4;
 constexpr int kCyc = 4;   // K steps per cycle of code loads
 
+// maximum over the wavefront (all 64 lanes must be active)
+__device__ inline float nv_wave_max(float m) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  return m;
+}
+
 // Workgroup (K group kg, tile group tg) of 4 wavefronts (four workgroups per
 // compute unit).  The K group's
 // slice of x (all B rows, KCR = 8 KC8 steps of 64 columns) is staged once in
@@ -122,16 +129,34 @@ __global__ __launch_bounds__(256) void nvfp4_gemv_kernel(const uint16_t* __restr
   if (threadIdx.x < 32) s_max[threadIdx.x] = 0u;
   for (int i = threadIdx.x; i < kRow / 2; i += blockDim.x) reinterpret_cast<uint32_t*>(xs + B * kRow)[i] = 0u;
   __syncthreads();
+  // Eight loads in flight per thread before any is used (a load followed by
+  // its use in every iteration would pay the memory latency per piece).  A
+  // row holds a multiple of 64 pieces, so the 64 pieces of a wavefront's
+  // load u all belong to one row: one LDS atomic per wavefront and load.
   const int per_row = KCR * 64 / 8;                   // 8-element pieces per batch row
-  for (int p = threadIdx.x; p < B * per_row; p += blockDim.x) {
-    const int b = p / per_row, e = (p - b * per_row) * 8;
-    uint4_t v{0u, 0u, 0u, 0u};
-    if (k0 + e < K) v = *reinterpret_cast<const uint4_t*>(x + (int64_t)b * K + k0 + e);   // K % 16 == 0
-    float m = 0.0f;
+  constexpr int kStageBatch = 8;
+  for (int p0 = threadIdx.x; p0 < B * per_row; p0 += kStageBatch * (int)blockDim.x) {
+    uint4_t v[kStageBatch];
 #pragma unroll
-    for (int w4 = 0; w4 < 4; ++w4) m = fmaxf(m, fmaxf(fabsf(bf16_lo(v[w4])), fabsf(bf16_hi(v[w4]))));
-    atomicMax(&s_max[b], __float_as_uint(m));
-    *reinterpret_cast<uint4_t*>(xs + b * kRow + e) = v;   // raw bf16 for now
+    for (int u = 0; u < kStageBatch; ++u) {
+      const int p = p0 + u * (int)blockDim.x;
+      const int b = p / per_row, e = (p - b * per_row) * 8;
+      v[u] = uint4_t{0u, 0u, 0u, 0u};
+      if (p < B * per_row && k0 + e < K)
+        v[u] = *reinterpret_cast<const uint4_t*>(x + (int64_t)b * K + k0 + e);   // K % 16 == 0
+    }
+#pragma unroll
+    for (int u = 0; u < kStageBatch; ++u) {
+      const int p = p0 + u * (int)blockDim.x;
+      if (p - lane >= B * per_row) break;             // uniform: the wavefront's pieces are all past the end
+      const int b = p / per_row, e = (p - b * per_row) * 8;
+      float m = 0.0f;
+#pragma unroll
+      for (int w4 = 0; w4 < 4; ++w4) m = fmaxf(m, fmaxf(fabsf(bf16_lo(v[u][w4])), fabsf(bf16_hi(v[u][w4]))));
+      m = nv_wave_max(m);
+      if (lane == 0) atomicMax(&s_max[b], __float_as_uint(m));
+      *reinterpret_cast<uint4_t*>(xs + b * kRow + e) = v[u];   // raw bf16 for now
+    }
   }
   __syncthreads();
   if (threadIdx.x < (unsigned)B) {
@@ -223,12 +248,6 @@ __global__ __launch_bounds__(256) void nvfp4_gemv_kernel(const uint16_t* __restr
 // sums in LDS.  After the one barrier, the kKsWaves partials of each (batch
 // row, tile row) are added in wavefront order and stored (deterministic).
 
-
-__device__ inline float nv_wave_max(float m) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-  return m;
-}
 
 template <int kKsWaves>
 __global__ __launch_bounds__(64 * kKsWaves) void nvfp4_gemv_ks_kernel(
