@@ -357,8 +357,43 @@ __device__ __forceinline__ void mx_gemm_tile(int64_t blk, const MxPanels& P, con
 
   // Block (i, j) holds, in lane l, output row m0 + 32i + l%32 and columns
   // n0 + 32j + 8g + 4(l/32) + t in register 4g + t (g, t = 0..3): four
-  // consecutive columns, stored as one 8-byte (bf16) or 16-byte (fp32) write
-  // when the row stride keeps them aligned (N % 4 == 0).
+  // consecutive columns.
+  //
+  // bf16 output of a wavefront tile inside Y (N % 8 == 0): each 32-row block
+  // goes through LDS (8-byte writes in the accumulator layout, 16-byte reads
+  // along the rows) so that every store instruction writes whole 128-byte
+  // lines; written straight from the accumulators, each instruction touches
+  // 32 lines with 16 bytes each and the stores of a tile (issued by all
+  // workgroups at about the same time) took ~7 % of the kernel at M = 32768.
+  // The LDS ring is free once every wavefront has drained its loads.
+  if constexpr (OUT == 1) {
+    __syncthreads();
+    constexpr int RS = 64 * TN + 16;                  // LDS bytes per staged row (pad staggers banks)
+    constexpr int LPR = 4 * TN;                       // lanes per row in the read-back (16 bytes each)
+    if (m0 + 32 * TM <= M && n0 + 32 * TN <= N && (N & 7) == 0) {
+      uint8_t* ep = smem + (size_t)wave * 32 * RS;
+      const int rl = lane & 31, h = lane >> 5;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const uint32_t b0 = f32_to_bf16_rne(acc[i][j][4 * g]), b1 = f32_to_bf16_rne(acc[i][j][4 * g + 1]);
+            const uint32_t b2 = f32_to_bf16_rne(acc[i][j][4 * g + 2]), b3 = f32_to_bf16_rne(acc[i][j][4 * g + 3]);
+            *reinterpret_cast<uint2_t*>(ep + rl * RS + (32 * j + 8 * g + 4 * h) * 2) =
+                uint2_t{b0 | (b1 << 16), b2 | (b3 << 16)};
+          }
+#pragma unroll
+        for (int r0 = 0; r0 < 32; r0 += 64 / LPR) {
+          const int rr = r0 + lane / LPR, seg = lane % LPR;
+          const uint4_t v = *reinterpret_cast<const uint4_t*>(ep + rr * RS + seg * 16);
+          *reinterpret_cast<uint4_t*>(reinterpret_cast<uint16_t*>(Y) + (m0 + 32 * i + rr) * N + n0 + seg * 8) = v;
+        }
+      }
+      return;
+    }
+  }
   const bool vec = (N & 3) == 0;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
