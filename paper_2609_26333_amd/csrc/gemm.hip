@@ -343,6 +343,39 @@ __device__ __forceinline__ void gemm_tile(
   // meet, producing output feature (n0 + 32j)/2 + 8g + 4h + t.
   const float gs = (*Ga) * (*Gw);
   const int h = lane >> 5;
+  if constexpr (OUT == kOutBF16 && !SW) {
+    // A full wave tile leaves through LDS: each store instruction then writes
+    // whole 128-byte rows instead of 16 bytes of each of 32 rows.  The barrier
+    // covers the other waves' last LDS reads and direct loads into the ring.
+    __syncthreads();
+    constexpr int RS = 64 * TN + 16;   // LDS bytes per staged row (the pad staggers banks)
+    constexpr int LPR = 4 * TN;        // lanes per row in the read-back (16 bytes each)
+    if (m0 + 32 * TM <= M && n0 + 32 * TN <= out.Nout && (out.Nout & 7) == 0) {
+      uint8_t* ep = smem + (size_t)wave * 32 * RS;
+      const int rl = lane & 31;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            uint32_t b[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) b[t] = f32_to_bf16_rne(acc[i][j][4 * g + t] * gs);
+            *reinterpret_cast<uint2_t*>(ep + rl * RS + (32 * j + 8 * g + 4 * h) * 2) =
+                uint2_t{b[0] | (b[1] << 16), b[2] | (b[3] << 16)};
+          }
+#pragma unroll
+        for (int r0 = 0; r0 < 32; r0 += 64 / LPR) {
+          const int rr = r0 + lane / LPR, seg = lane % LPR;
+          const uint4_t v = *reinterpret_cast<const uint4_t*>(ep + rr * RS + seg * 16);
+          *reinterpret_cast<uint4_t*>(reinterpret_cast<uint16_t*>(out.Y) + (m0 + 32 * i + rr) * out.Nout + n0 +
+                                      seg * 8) = v;
+        }
+      }
+      return;
+    }
+  }
   if constexpr (OUT != kOutNvfp4) {
     const bool vec = (out.Nout & 3) == 0;
 #pragma unroll
