@@ -151,7 +151,8 @@ def _upload_nvfp4(q, c, G):
     return t
 
 
-GEMM_SHAPES = [(128, 512, 512), (100, 72, 48), (1, 1, 16), (300, 520, 1024), (257, 33, 64), (64, 256, 4096)]
+GEMM_SHAPES = [(128, 512, 512), (100, 72, 48), (1, 1, 16), (300, 520, 1024), (257, 33, 64), (64, 256, 4096),
+               (200, 132, 128), (520, 392, 256)]
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
