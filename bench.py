@@ -209,7 +209,7 @@ def cpu_baseline(w_down, X, G_x, min_seconds=10.0):
 
     import synth
     from oracle import linalg, lut, nvfp4
-    cfg = synth.CONFIGS[4]
+    cfg = synth.STACK_27B_M32768
     qw, cw, Gw = nvfp4.quantize_dynamic(w_down)
     w_hat = nvfp4.dequantize(qw, cw, Gw)
     codes, table = lut.quantize_per_row(w_down, 3)
@@ -306,7 +306,7 @@ def run(args, clk_path):
     ev = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
 
     # ---------------------------------------------------------------- prefill inputs
-    cfg = synth.CONFIGS[4]
+    cfg = synth.STACK_27B_M32768
     layers = {l.name: l for l in cfg.layers}
     down = layers["down"]
     M, N, K = cfg.m, down.n, down.k
@@ -449,15 +449,15 @@ def run(args, clk_path):
         del stacks
         torch.cuda.empty_cache()
         out["mxfp4_prefill_m32768"] = mxfp4_prefill(dq, torch, lib, s, sp, w_down, X, M, N, K)
-        c1 = synth.CONFIGS[1]
-        up = c1.layers[0]
-        out["mxfp4_prefill_8b_up_m2048"] = mxfp4_prefill(dq, torch, lib, s, sp, synth.layer_weight(c1, up),
-                                                         dev(synth.prefill_x(c1, up.k).view(np.int16)), c1.m,
+        up8b = synth.UP_8B_M2048
+        up = up8b.layers[0]
+        out["mxfp4_prefill_8b_up_m2048"] = mxfp4_prefill(dq, torch, lib, s, sp, synth.layer_weight(up8b, up),
+                                                         dev(synth.prefill_x(up8b, up.k).view(np.int16)), up8b.m,
                                                          up.n, up.k, reps=100)
         del A, Y, X
         torch.cuda.empty_cache()
-        out["c2_fused_m8192"] = c2_fused(dq, synth, torch, np, lib, s, sp)
-        out["c3_block_chain_m4096"] = c3_chain(dq, synth, torch, np, lib, s, sp)
+        out["fused_down_27b_m8192"] = fused_down_m8192(dq, synth, torch, np, lib, s, sp)
+        out["block_chain_27b_m4096"] = block_chain_m4096(dq, synth, torch, np, lib, s, sp)
         out["nvfp4a16_decode_27b_down"] = nvfp4a16_decode(dq, torch, lib, s, sp, Wq, N, K)
         out["rmsnorm_quant_27b_hidden"] = rmsnorm_quant(dq, synth, torch, np, lib, s, sp)
     if not args.no_cpu_baseline:
@@ -572,11 +572,11 @@ def mxfp4_prefill(dq, torch, lib, s, sp, w, X, M, N, K, reps=5):
             "note": "MXFP4 W4A4 (E2M1, E8M0 per 32 along K) on the scaled FP4 MFMA; same shapes, bf16 output"}
 
 
-def c2_fused(dq, synth, torch, np, lib, s, sp):
+def fused_down_m8192(dq, synth, torch, np, lib, s, sp):
     """27B MLP down-projection at an 8K prompt: M = 8192, K = 17408, N = 5120,
     activation quantization fused into the prefill call (static scale, the
     NVFP4 copy of X in a caller workspace)."""
-    cfg = synth.CONFIGS[2]
+    cfg = synth.DOWN_27B_M8192
     layer = cfg.layers[0]
     M, N, K = cfg.m, layer.n, layer.k
     W = dq.dq_pack_nvfp4(torch.from_numpy(synth.layer_weight(cfg, layer)).cuda())
@@ -606,12 +606,12 @@ def c2_fused(dq, synth, torch, np, lib, s, sp):
                     "quant_pass_us and gemm_alone_us time the two halves alone"}
 
 
-def c3_chain(dq, synth, torch, np, lib, s, sp):
+def block_chain_m4096(dq, synth, torch, np, lib, s, sp):
     """The 27B block's linears chained on one stream at M = 4096: activation
     quantization and q/k/v (bf16 out); quantization of the attention-output
     stand-in and o with an NVFP4 epilogue (static scale) feeding gate/up with
     SwiGLU and an NVFP4 epilogue feeding down (bf16 out)."""
-    cfg = synth.CONFIGS[3]
+    cfg = synth.BLOCK_27B_M4096
     L = {l.name: l for l in cfg.layers}
     M = cfg.m
     W = {n: dq.dq_pack_nvfp4(torch.from_numpy(synth.layer_weight(cfg, L[n])).cuda()) for n in L}
@@ -654,7 +654,7 @@ def rmsnorm_quant(dq, synth, torch, np, lib, s, sp):
     """RMSNorm fused with the NVFP4 activation quantizer (static scale) on the
     27B hidden state at M = 4096 and M = 32768, K = 5120, next to the plain
     activation quantizer of the same tensor."""
-    cfg = synth.CONFIGS[3]
+    cfg = synth.BLOCK_27B_M4096
     K = 5120
     out = {}
     X0 = torch.from_numpy(synth.prefill_x(cfg, K).view(np.int16)).cuda()

@@ -83,9 +83,9 @@ def nvfp4_rows(t, rows):
     return q[pick], c[pick]
 
 
-CFG4 = synth.CONFIGS[4]
-CFG3 = synth.CONFIGS[3]
-LAYERS = {l.name: l for l in CFG4.layers}
+STACK = synth.STACK_27B_M32768
+BLOCK = synth.BLOCK_27B_M4096
+LAYERS = {l.name: l for l in STACK.layers}
 
 
 def sample_rows(n, count, seed):
@@ -102,7 +102,7 @@ _W_CACHE = {}
 def layer_weight(name):
     if name not in _W_CACHE:
         _W_CACHE.clear()
-        _W_CACHE[name] = synth.layer_weight(CFG4, LAYERS[name])
+        _W_CACHE[name] = synth.layer_weight(STACK, LAYERS[name])
     return _W_CACHE[name]
 
 
@@ -123,7 +123,7 @@ def test_lut_gemv_27b_block(name, bits):
     assert np.array_equal(codes, codes_ref), f"codes differ at {np.argwhere(codes != codes_ref)[:5]}"
     w_hat = lut.dequantize_per_row(codes_ref, table_ref)
     for B in (1, 8, 16):
-        xb = synth.decode_x(CFG4, K, B)
+        xb = synth.decode_x(STACK, K, B)
         x = bf16_dev(xb)
         ws_n = dq.dq_decode_gemv_workspace_size(B, Wq)
         ws = torch.empty(max(ws_n, 16), dtype=torch.uint8, device="cuda")
@@ -147,19 +147,19 @@ def _calibrated_scale(cfg, K):
 
 
 @pytest.fixture(scope="module")
-def c4_prefill():
+def stack_prefill():
     layer = LAYERS["down"]
-    say("c4 prefill: generating X [32768, 17408] and W [5120, 17408]")
-    w = synth.layer_weight(CFG4, layer)
-    xb = synth.prefill_x(CFG4, layer.k)
-    return w, xb, _calibrated_scale(CFG4, layer.k)
+    say("M = 32768 prefill: generating X [32768, 17408] and W [5120, 17408]")
+    w = synth.layer_weight(STACK, layer)
+    xb = synth.prefill_x(STACK, layer.k)
+    return w, xb, _calibrated_scale(STACK, layer.k)
 
 
-def test_nvfp4_gemm_m32768_sampled(c4_prefill):
+def test_nvfp4_gemm_m32768_sampled(stack_prefill):
     """The NVFP4 prefill GEMM of the decode-sweep workload (M = 32768 tokens on
     the 27B down-projection), as the benchmark runs it: static-scale
     activation quantization, then the GEMM with bf16 output."""
-    w, xb, G_x = c4_prefill
+    w, xb, G_x = stack_prefill
     M, K = xb.shape
     N = w.shape[0]
     W = dq.dq_pack_nvfp4(dev(w))
@@ -183,8 +183,8 @@ def test_nvfp4_gemm_m32768_sampled(c4_prefill):
     PB.assert_within(y, ref, PB.fp32_sum_bound(PB.abs_products(a_hat, w_hat), K), "nvfp4 gemm M=32768", bf16=True)
 
 
-def test_mxfp4_gemm_m32768_sampled(c4_prefill):
-    w, xb, _ = c4_prefill
+def test_mxfp4_gemm_m32768_sampled(stack_prefill):
+    w, xb, _ = stack_prefill
     M, K = xb.shape
     N = w.shape[0]
     Wm = dq.dq_pack_mxfp4(dev(w))
@@ -212,20 +212,20 @@ def test_block_chain_27b_m4096_per_step():
     gate/up with SwiGLU requantized for down, down with bf16 output.  Each
     step on sampled rows and output blocks against the oracle, from the GPU's
     own input codes."""
-    L3 = {l.name: l for l in CFG3.layers}
-    M = CFG3.m
+    L3 = {l.name: l for l in BLOCK.layers}
+    M = BLOCK.m
     rng = np.random.default_rng(303)
     rows = np.sort(np.concatenate([rng.choice(M, 6, replace=False), [0, M - 1]]))
     rows_t = torch.from_numpy(rows).cuda()
 
     def weight(name):
-        w = synth.layer_weight(CFG3, L3[name])
+        w = synth.layer_weight(BLOCK, L3[name])
         return w, dq.dq_pack_nvfp4(dev(w))
 
     # q/k/v
     say("chain: qkv")
-    xb = synth.prefill_x(CFG3, 5120)
-    G_x = _calibrated_scale(CFG3, 5120)
+    xb = synth.prefill_x(BLOCK, 5120)
+    G_x = _calibrated_scale(BLOCK, 5120)
     w_qkv, W_qkv = weight("qkv")
     A = dq.dq_quantize_act_nvfp4(bf16_dev(xb), G_static=g_dev(G_x))
     Y_qkv = dq.dq_prefill_gemm(W_qkv, A=A, out_kind=dq.OUT_BF16)
@@ -243,7 +243,7 @@ def test_block_chain_27b_m4096_per_step():
     # o, with NVFP4 requantization for the next layer; its static output scale
     # is calibrated on the oracle's result for the sampled rows
     say("chain: o")
-    ab = synth.attn_out_standin(CFG3, M, 5120)
+    ab = synth.attn_out_standin(BLOCK, M, 5120)
     G_a = nvfp4.global_scale(nvfp4.amax(formats.f32_from_bf16_bits(ab[:512])))
     w_o, W_o = weight("o")
     qa, ca, _ = nvfp4.quantize_bf16_activations(ab[rows], G_a)

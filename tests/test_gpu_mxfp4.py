@@ -158,11 +158,11 @@ def test_mx_gemm_exact_small_scales():
     assert np.array_equal(y.astype(np.float64), ref)
 
 
-def test_mx_gemm_end_to_end_c1_sampled_rows():
+def test_mx_gemm_end_to_end_8b_up_sampled_rows():
     """The 8B up-projection at full size (M=2048, K=4096, N=12288) through the
     GPU quantizers and GEMM in the benchmark's launch configuration; 48 rows
     of the bf16 output checked against the oracle."""
-    cfg = synth.CONFIGS[1]
+    cfg = synth.UP_8B_M2048
     layer = cfg.layers[0]
     w = synth.layer_weight(cfg, layer)
     xb = synth.prefill_x(cfg, layer.k)
@@ -175,10 +175,10 @@ def test_mx_gemm_end_to_end_c1_sampled_rows():
     ref = linalg.mxfp4_gemm(qa, sa, qw, sw)
     y = host(Y[torch.from_numpy(rows).cuda()].float()).astype(np.float64)
     err = linalg.rel_fro(y, formats.bf16_rne_from_f64(ref))
-    say("  c1 sampled rel_fro", err)
+    say("  8B up sampled rel_fro", err)
     assert err <= TOL
     bound = PB.fp32_sum_bound(PB.abs_products(mxfp4.dequantize(qa, sa), mxfp4.dequantize(qw, sw)), layer.k)
-    PB.assert_within(y, ref, bound, "mx c1 gemm", bf16=True)
+    PB.assert_within(y, ref, bound, "mx 8B up gemm", bf16=True)
 
 
 @pytest.mark.parametrize("M,N,K", [(0, 64, 64), (64, 0, 64), (40, 24, 0)])

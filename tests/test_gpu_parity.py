@@ -193,11 +193,11 @@ def test_gemm_exact_unit_scales():
     assert np.array_equal(y.astype(np.float64), ref)
 
 
-def test_gemm_end_to_end_c1_sampled_rows():
+def test_gemm_end_to_end_8b_up_sampled_rows():
     """The 8B up-projection at full size (M=2048, K=4096, N=12288) through the
     GPU quantizers and GEMM in the benchmark's launch configuration; 48 rows
     of the output checked against the oracle."""
-    cfg = synth.CONFIGS[1]
+    cfg = synth.UP_8B_M2048
     layer = cfg.layers[0]
     w = synth.layer_weight(cfg, layer)
     xb = synth.prefill_x(cfg, layer.k)
@@ -212,10 +212,10 @@ def test_gemm_end_to_end_c1_sampled_rows():
     ref = linalg.nvfp4_gemm(qa, ca, G_x, qw, cw, Gw)
     y = host(Y[torch.from_numpy(rows).cuda()].float()).astype(np.float64)
     err = linalg.rel_fro(y, formats.bf16_rne_from_f64(ref))
-    say("  c1 sampled rel_fro", err)
+    say("  8B up sampled rel_fro", err)
     assert err <= TOL
     bound = PB.fp32_sum_bound(PB.abs_products(nvfp4.dequantize(qa, ca, G_x), nvfp4.dequantize(qw, cw, Gw)), layer.k)
-    PB.assert_within(y, ref, bound, "c1 gemm", bf16=True)
+    PB.assert_within(y, ref, bound, "8B up gemm", bf16=True)
 
 
 @pytest.mark.parametrize("M,N,K,out", [(2048, 10240, 256, "bf16"), (1024, 20480, 128, "nvfp4"),
@@ -297,12 +297,12 @@ def test_gemm_fused_act_quant(M, N, K):
         assert torch.equal(q_f.G, q_u.G)
 
 
-def test_gemm_fused_c2_full_size_sampled():
+def test_gemm_fused_down_27b_full_size_sampled():
     """The 27B-class down projection with fused activation quantization
     (M=8192, K=17408, N=5120) at full size; sampled rows and columns of the
     bf16 output against the oracle (weights quantized with the whole
     tensor's global scale)."""
-    cfg = synth.CONFIGS[2]
+    cfg = synth.DOWN_27B_M8192
     layer = cfg.layers[0]
     w = synth.layer_weight(cfg, layer)
     xb = synth.prefill_x(cfg, layer.k)
@@ -319,10 +319,10 @@ def test_gemm_fused_c2_full_size_sampled():
     ref = linalg.nvfp4_gemm(qa, ca, G_x, qw, cw, Gw)
     y = host(Y[torch.from_numpy(rows).cuda()][:, torch.from_numpy(cols).cuda()].float()).astype(np.float64)
     err = linalg.rel_fro(y, formats.bf16_rne_from_f64(ref))
-    say("  c2 fused sampled rel_fro", err)
+    say("  fused down sampled rel_fro", err)
     assert err <= TOL
     bound = PB.fp32_sum_bound(PB.abs_products(nvfp4.dequantize(qa, ca, G_x), nvfp4.dequantize(qw, cw, Gw)), layer.k)
-    PB.assert_within(y, ref, bound, "c2 fused gemm", bf16=True)
+    PB.assert_within(y, ref, bound, "fused down gemm", bf16=True)
 
 
 def test_gemm_empty():
