@@ -259,10 +259,12 @@ def test_gemm_tile_geometries_agree(M, N, K, out):
         qa, ca, _ = nvfp4.quantize_bf16_activations(xb[rows], G_x)
         qw, cw, Gw = nvfp4.quantize_dynamic(w)
         ref = linalg.nvfp4_gemm(qa, ca, G_x, qw, cw, Gw)
-        y = full[rows].view(np.uint16)
-        err = linalg.rel_fro(formats.f64_from_bf16_bits(y), formats.bf16_rne_from_f64(ref))
+        y = formats.f64_from_bf16_bits(full[rows].view(np.uint16))
+        err = linalg.rel_fro(y, formats.bf16_rne_from_f64(ref))
         say("  sampled rel_fro", err)
         assert err <= TOL
+        bound = PB.fp32_sum_bound(PB.abs_products(nvfp4.dequantize(qa, ca, G_x), nvfp4.dequantize(qw, cw, Gw)), K)
+        PB.assert_within(y, ref, bound, "geometries bf16", bf16=True)
 
 
 FUSED_SHAPES = [(128, 512, 512), (300, 520, 1024), (1, 16, 64), (0, 32, 64)]
@@ -287,7 +289,10 @@ def test_gemm_fused_act_quant(M, N, K):
     if M:
         qa, ca, _ = nvfp4.quantize_bf16_activations(xb, G_x)
         qw, cw, Gw = nvfp4.quantize_dynamic(w)
-        assert linalg.rel_fro(y_f, linalg.nvfp4_gemm(qa, ca, G_x, qw, cw, Gw)) <= TOL
+        ref = linalg.nvfp4_gemm(qa, ca, G_x, qw, cw, Gw)
+        assert linalg.rel_fro(y_f, ref) <= TOL
+        bound = PB.fp32_sum_bound(PB.abs_products(nvfp4.dequantize(qa, ca, G_x), nvfp4.dequantize(qw, cw, Gw)), K)
+        PB.assert_within(y_f, ref, bound, "fused gemm")
     if N % 16 == 0:
         G_o = dev(np.array([0.01], np.float32))
         q_f = dq.dq_prefill_gemm(W, X=bf16_dev(xb), G_x_static=Gd, out_kind=dq.OUT_NVFP4, G_out_static=G_o)
@@ -417,6 +422,8 @@ def test_gemv_large_activations_rescaled():
     y = host(dq.dq_decode_gemv(bf16_dev(xb), Wq))
     for b in range(2):
         assert linalg.rel_fro(y[b], ref[b]) <= TOL
+    PB.assert_within(y, ref, PB.gemv_bound(formats.f64_from_bf16_bits(xb), lut.dequantize_per_row(codes_ref, lut_ref), K),
+                     "rescaled activations gemv")
 
 
 def test_gemv_workspace_and_pool_paths_agree():
@@ -440,7 +447,10 @@ def test_gemv_workspace_and_pool_paths_agree():
                               torch.cuda.current_stream().cuda_stream) == dq.DQ_OK
     assert torch.equal(y_ws, y_pool) and torch.equal(y_ws, y_ws2)
     codes_ref, lut_ref = lut.quantize_per_row(w, 3)
-    assert linalg.rel_fro(host(y_ws), linalg.lut_gemv_per_row(xb, codes_ref, lut_ref)) <= TOL
+    ref = linalg.lut_gemv_per_row(xb, codes_ref, lut_ref)
+    assert linalg.rel_fro(host(y_ws), ref) <= TOL
+    PB.assert_within(host(y_ws), ref, PB.gemv_bound(formats.f64_from_bf16_bits(xb),
+                                                    lut.dequantize_per_row(codes_ref, lut_ref), K), "workspace gemv")
 
 
 # ---------------------------------------------------------------- NVFP4A16 decode GEMV
@@ -526,7 +536,10 @@ def test_lut_autocast_to_nvfp4(N, K, bits, mode):
         qa, ca, Ga = nvfp4.quantize_bf16_activations(xb)
         A = _upload_nvfp4(qa, ca, Ga)
         y = host(dq.dq_prefill_gemm(Wn, A=A, out_kind=dq.OUT_F32))
-        assert linalg.rel_fro(y, linalg.nvfp4_gemm(qa, ca, Ga, q_ref, c_ref, G_ref)) <= TOL
+        ref = linalg.nvfp4_gemm(qa, ca, Ga, q_ref, c_ref, G_ref)
+        assert linalg.rel_fro(y, ref) <= TOL
+        bound = PB.fp32_sum_bound(PB.abs_products(nvfp4.dequantize(qa, ca, Ga), nvfp4.dequantize(q_ref, c_ref, G_ref)), K)
+        PB.assert_within(y, ref, bound, "autocast gemm")
 
 
 def test_lut_autocast_static_scale():

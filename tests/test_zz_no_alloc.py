@@ -12,9 +12,10 @@ import pytest
 import torch
 
 sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import parity_bounds as PB  # noqa: E402
 
 import synth  # noqa: E402
-from oracle import linalg, lut  # noqa: E402
+from oracle import formats, linalg, lut  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -60,7 +61,11 @@ def test_noalloc_gemv_matches_workspace_gemv_twice_then_batch1():
     assert 0 < n1 <= dq.NOALLOC_SCRATCH_BYTES
     assert torch.equal(y_ref, y_na)
     codes, table = lut.quantize_per_row(w, 3)
-    assert linalg.rel_fro(y_na.cpu().numpy(), linalg.lut_gemv_per_row(xb, codes, table)) <= 1e-3
+    ref = linalg.lut_gemv_per_row(xb, codes, table)
+    assert linalg.rel_fro(y_na.cpu().numpy(), ref) <= 1e-3
+    PB.assert_within(y_na.cpu().numpy(), ref,
+                     PB.gemv_bound(formats.f64_from_bf16_bits(xb), lut.dequantize_per_row(codes, table), 5120),
+                     "noalloc gemv")
     # second call, smaller: batch 4 on a 1040 x 4096 weight, bf16 output; the scratch still
     # holds the first call's partial sums, which must not leak into this result
     _, Wq2, x2, _ = _case(1040, 4096, 4, 402)
