@@ -1241,10 +1241,15 @@ hipError_t launch_gemv_t(const uint16_t* x, int64_t B, const LutView& w, int out
       }
       // rounds: one per resident workgroup slot, every workgroup running the
       // same number (a partial last round would leave few wavefronts
-      // streaming at the end)
+      // streaming at the end).  At most four workgroups per compute unit:
+      // wavefronts start at about two per nanosecond over the whole chip, so
+      // the 27B gate/up matrix (2176 row tiles) ran 3-4 % faster as 726
+      // workgroups of three rounds than as 1088 of two; smaller matrices keep
+      // one round either way.
       int64_t rounds = 1;
       for (int it = 0; it < 3; ++it) {
-        const int per_cu = persist_wgs_per_cu(vgprs.load(std::memory_order_relaxed), kW, lds_of(rounds));
+        const int per_cu =
+            std::min(4, persist_wgs_per_cu(vgprs.load(std::memory_order_relaxed), kW, lds_of(rounds)));
         const int64_t gmax = std::max<int64_t>(1, (int64_t)num_cus() * per_cu);
         rounds = (pl.tiles + gmax - 1) / gmax;
       }
