@@ -21,7 +21,9 @@
 //  * operands stay compressed (4.5 bits/element) until they reach registers:
 //    an LDS ring of up to six stages (one 64-column K step each: raw code tiles of
 //    1 KiB and E4M3 scale tiles of 128 bytes) is filled by direct
-//    global->LDS loads as many steps ahead; one workgroup barrier per step;
+//    global->LDS buffer loads as many steps ahead (a buffer resource per
+//    operand row panel: per load a fixed lane offset, per step one scalar
+//    offset, no address arithmetic in the loop); one workgroup barrier per step;
 //  * within a stage, a 32x64 code tile is one contiguous KiB; the loading
 //    lane i fetches 16-byte chunk 2*(i%32) + i/32 so that the consuming lane
 //    l (row l%32, columns 32*(l/32)..+31) reads LDS bytes 16l..16l+15
@@ -36,6 +38,7 @@
 //  * output tiles are handed out in bands of row panels, each XCD taking a
 //    compact sub-block of the tiles in flight (gemm_tile_of).
 #include <algorithm>
+#include <climits>
 #include <type_traits>
 
 #include "dq_device.hpp"
@@ -178,40 +181,57 @@ __device__ __forceinline__ void gemm_tile(
   // reload the last one into a slot that is no longer read, so every step
   // issues the same loads (no branches in the main loop).
   const int chunk = 2 * (lane & 31) + (lane >> 5);
-  const uint8_t* c_src[CPW];
+  // Buffer resources based at this workgroup's first row tile of each
+  // operand (offsets stay below at * KT * 1024 bytes, far inside 31 bits);
+  // per load a fixed lane offset, per K step one scalar offset.
+  auto rsrc = [](const uint8_t* base, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), 0, (int)bytes, 0x00020000);
+  };
+  const __amdgpu_buffer_rsrc_t rac = rsrc(a_codes + a_tr0 * KT * 1024, (int64_t)Gm::at * KT * 1024);
+  const __amdgpu_buffer_rsrc_t rwc = rsrc(w_codes + w_tr0 * KT * 1024, (int64_t)Gm::wt * KT * 1024);
+  const __amdgpu_buffer_rsrc_t ras = rsrc(a_scales + a_tr0 * KT * 128, (int64_t)Gm::at * KT * 128);
+  const __amdgpu_buffer_rsrc_t rws = rsrc(w_scales + w_tr0 * KT * 128, (int64_t)Gm::wt * KT * 128);
+  uint32_t c_off[CPW];
+  bool c_a[CPW];
   int c_dst[CPW];
 #pragma unroll
   for (int u = 0; u < CPW; ++u) {
     const int t = wave + Gm::waves * u;
     const bool is_a = t < Gm::at;
     const int b = is_a ? t : t - Gm::at;
-    const int64_t tr = min((is_a ? a_tr0 : w_tr0) + b, (is_a ? a_tiles_r : w_tiles_r) - 1);
-    c_src[u] = (is_a ? a_codes : w_codes) + tr * KT * 1024 + chunk * 16;
+    const int64_t tr = min((is_a ? a_tr0 : w_tr0) + b, (is_a ? a_tiles_r : w_tiles_r) - 1) - (is_a ? a_tr0 : w_tr0);
+    c_a[u] = is_a;
+    c_off[u] = (uint32_t)(tr * KT * 1024 + chunk * 16);
     c_dst[u] = (is_a ? Gm::a_codes : Gm::w_codes) + b * 1024;
   }
-  const uint8_t* s_src[SPW];
+  uint32_t s_off[SPW];
+  bool s_a[SPW];
   int s_dst[SPW];
 #pragma unroll
   for (int u = 0; u < SPW; ++u) {
     const int idx = min(wave + Gm::waves * u, Gm::scale_loads - 1);
     const int t = 2 * idx + (lane >> 5);
-    const bool is_a = t < Gm::at;
+    const bool is_a = 2 * idx < Gm::at;   // both tiles of a pair belong to one operand (at is even)
     const int b = is_a ? t : t - Gm::at;
-    const int64_t tr = min((is_a ? a_tr0 : w_tr0) + b, (is_a ? a_tiles_r : w_tiles_r) - 1);
-    s_src[u] = (is_a ? a_scales : w_scales) + tr * KT * 128 + (lane & 31) * 4;
+    const int64_t tr = min((is_a ? a_tr0 : w_tr0) + b, (is_a ? a_tiles_r : w_tiles_r) - 1) - (is_a ? a_tr0 : w_tr0);
+    s_a[u] = is_a;
+    s_off[u] = (uint32_t)(tr * KT * 128 + (lane & 31) * 4);
     s_dst[u] = Gm::a_scales + idx * 256;
   }
-  auto issue = [&](int kt) {
-    uint8_t* stage = smem + (kt % S) * Gm::bytes;
+  // stage kt into ring slot `slot` (kt past the end: the last one again)
+  auto issue = [&](int kt, int slot) {
+    uint8_t* stage = smem + slot * Gm::bytes;
     const int ktc = kt < KTi ? kt : KTi - 1;
 #pragma unroll
     for (int u = 0; u < CPW; ++u)
-      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(c_src[u] + (size_t)ktc * 1024),
-                                       reinterpret_cast<void*>(stage + c_dst[u]), 16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(c_a[u] ? rac : rwc,
+                                               (__attribute__((address_space(3))) void*)(stage + c_dst[u]), 16,
+                                               c_off[u], ktc * 1024, 0, 0);
 #pragma unroll
     for (int u = 0; u < SPW; ++u)
-      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(s_src[u] + (size_t)ktc * 128),
-                                       reinterpret_cast<void*>(stage + s_dst[u]), 4, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(s_a[u] ? ras : rws,
+                                               (__attribute__((address_space(3))) void*)(stage + s_dst[u]), 4,
+                                               s_off[u], ktc * 128, 0, 0);
   };
 
   float16_t acc[TM][TN];
@@ -257,7 +277,7 @@ __device__ __forceinline__ void gemm_tile(
   if (KTi > 0) {
     // prologue: stages 0 .. S-1 in flight, stage 0 landed everywhere
 #pragma unroll
-    for (int st = 0; st < S; ++st) issue(st);
+    for (int st = 0; st < S; ++st) issue(st, st);
     wait_vm<(S - 1) * L>();
     lds_barrier();
     Raw R0, R1;
@@ -273,8 +293,9 @@ __device__ __forceinline__ void gemm_tile(
     // fences keep this order; the empty asm statements pin the accumulators
     // at the end of the step (the compiler would otherwise sink the MFMAs,
     // pure register operations, behind the next step's barrier).
-    auto step = [&](int kt, Raw& Rc, Raw& Rn) {
-      const uint8_t* stg_next = smem + ((kt + 1) % S) * Gm::bytes;
+    auto step = [&](int kt, Raw& Rc, Raw& Rn, int slot) {
+      const int nslot = slot + 1 == S ? 0 : slot + 1;
+      const uint8_t* stg_next = smem + nslot * Gm::bytes;
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
         Ops& Dc = (s & 1) ? D1 : D0;
@@ -288,7 +309,7 @@ __device__ __forceinline__ void gemm_tile(
           if (s == 0 && q == 1) {
             wait_vm<(S - 2) * L>();
             lds_barrier();
-            issue(kt + S);
+            issue(kt + S, slot);
             __builtin_amdgcn_sched_barrier(0);
           }
           if (s == 1) {
@@ -320,17 +341,21 @@ __device__ __forceinline__ void gemm_tile(
 #pragma unroll
       for (int u = 0; u < kTiles; ++u) dequant_one(R, 0, D0, u);
     };
-    int kt = 0;
+    int kt = 0, slot = 0;
+    auto adv = [&](int sl) { return sl + 1 == S ? 0 : sl + 1; };
     if (KTi & 1) {
       first(R1);
-      step(0, R1, R0);
+      step(0, R1, R0, 0);
       kt = 1;
+      slot = 1;
     } else {
       first(R0);
     }
     for (; kt < KTi; kt += 2) {
-      step(kt, R0, R1);
-      step(kt + 1, R1, R0);
+      step(kt, R0, R1, slot);
+      slot = adv(slot);
+      step(kt + 1, R1, R0, slot);
+      slot = adv(slot);
     }
     // drain the redundant reloads of the last steps before the workgroup ends
     wait_vm<0>();
@@ -500,6 +525,10 @@ hipError_t launch_geo(const GemmArgs& a, int64_t split, hipStream_t s) {
   const int64_t a_tiles_r = round_up(a.M, 32) / 32;
   const int64_t w_tiles_r = round_up(a.N, 32) / 32;
   const int64_t KT = round_up(a.K, 64) / 64;
+  // the loaders address one workgroup's row panel of an operand with 32-bit
+  // buffer offsets (at most 8 code tiles of KT KiB)
+  if ((int64_t)std::max(std::max(Gm::at, Gm::wt), std::max(Gh::at, Gh::wt)) * KT * 1024 > INT32_MAX)
+    return hipErrorNotSupported;
   const Panels big{(a.M + Gm::bm - 1) / Gm::bm, (split + Gm::bn - 1) / Gm::bn, 0};
   const Panels small{split < a.N ? (a.M + Gh::bm - 1) / Gh::bm : 0, (a.N - split + Gh::bn - 1) / Gh::bn, split};
   const int64_t blocks = big.tiles_m * big.tiles_n + small.tiles_m * small.tiles_n;
