@@ -230,7 +230,7 @@ dq_status dq_quantize_act_nvfp4(const uint16_t* X, int64_t M, int64_t K, const f
  * epilogue_flags DQ_EPI_SWIGLU: W rows are interleaved gate/up in groups of
  *   16 (rows 32j..32j+15 = gate rows 16j.., rows 32j+16..32j+31 = up rows
  *   16j..); the output column j = silu(gate_j) * up_j, N/2 columns.
- * K % 16 == 0, M >= 0, N >= 0; K < 2^24 (the kernel addresses a row panel of
+ * K % 16 == 0, M >= 0, N >= 0; K < 2^23 (the kernel addresses a row panel of
  * each operand with 32-bit offsets; larger K -> DQ_ERR_UNSUPPORTED). */
 dq_status dq_prefill_gemm_workspace_size(int64_t M, int64_t K, size_t* bytes);
 dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G_x_static,

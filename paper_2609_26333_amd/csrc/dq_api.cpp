@@ -306,7 +306,7 @@ dq_status dq_prefill_gemm(const dq_nvfp4_t* A, const uint16_t* X, const float* G
   dq_status st = check_nvfp4(W, "W", N, K);
   if (st != DQ_OK) return st;
   if (N < 0 || K < 0 || K % 16 != 0) return fail(DQ_ERR_INVALID_ARG, "W: rows >= 0 and cols %% 16 == 0 required");
-  if (K >= ((int64_t)1 << 24)) return fail(DQ_ERR_UNSUPPORTED, "K < 2^24 required (32-bit row-panel offsets)");
+  if (K >= ((int64_t)1 << 23)) return fail(DQ_ERR_UNSUPPORTED, "K < 2^23 required (32-bit row-panel offsets)");
   if (A != nullptr) {
     st = check_nvfp4(A, "A", M, K);
     if (st != DQ_OK) return st;

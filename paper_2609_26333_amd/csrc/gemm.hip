@@ -66,18 +66,29 @@ struct Geo {
   static constexpr int w_codes = at * 1024;
   static constexpr int a_scales = w_codes + wt * 1024;
   static constexpr int w_scales = a_scales + at * 128;
-  static constexpr int bytes = w_scales + wt * 128;
-  static constexpr int stages_fit = kLdsBudget / OCC / bytes;
-  static constexpr int stages = stages_fit < 6 ? stages_fit : 6;
   // direct loads per stage: one per code tile, one dword load per pair of scale tiles
   static constexpr int code_loads = at + wt;
   static constexpr int scale_loads = (at + wt) / 2;
   static constexpr int cpw = code_loads / waves;
   static constexpr int spw = (scale_loads + waves - 1) / waves;
+  // scale loads past the last pair land in padding after the W scales
+  static constexpr int spad = (waves * spw - scale_loads) * 256;
+  static constexpr int bytes = w_scales + wt * 128 + spad;
+  static constexpr int stages_fit = kLdsBudget / OCC / bytes;
+  static constexpr int stages = stages_fit < 6 ? stages_fit : 6;
   static constexpr int loads_per_wave = cpw + spw;
   static_assert(code_loads % waves == 0 && at % 2 == 0 && wt % 2 == 0, "uniform load distribution");
   static_assert(stages >= 4 && (stages - 1) * loads_per_wave <= 63, "LDS ring of four to six stages");
 };
+
+// f(integral_constant<int, U>) for U = B .. E - 1 (compile-time indices)
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
 
 // 8 E2M1 codes (one dword) times an fp16 block scale -> 8 exact fp16 values.
 __device__ inline half8_t dequant8(uint32_t w, half2_t s) {
@@ -173,9 +184,9 @@ __device__ __forceinline__ void gemm_tile(
   const int64_t n0 = n_off + bn * Gm::bn + wn * 32 * TN;
   const int KTi = (int)KT;
 
-  // Direct loads of one stage: code tiles t = wave + waves*u (A tiles first,
-  // then W); scale instruction idx covers tiles 2 idx (lanes 0..31) and
-  // 2 idx + 1 (lanes 32..63), waves past the last one repeating it.  Tiles
+  // Direct loads of one stage: code tiles t = wave*CPW + u (A tiles first,
+  // then W, contiguous in LDS); scale instruction idx covers tiles 2 idx
+  // (lanes 0..31) and 2 idx + 1 (lanes 32..63).  Tiles
   // past the end of an operand read its last row tile (in bounds): they only
   // feed output rows / columns that are never stored.  K steps past the end
   // reload the last one into a slot that is no longer read, so every step
@@ -183,55 +194,61 @@ __device__ __forceinline__ void gemm_tile(
   const int chunk = 2 * (lane & 31) + (lane >> 5);
   // Buffer resources based at this workgroup's first row tile of each
   // operand (offsets stay below at * KT * 1024 bytes, far inside 31 bits);
-  // per load a fixed lane offset, per K step one scalar offset.
+  // per load a fixed lane offset, per K step one scalar offset.  The bases
+  // sit kBias bytes lower, so that the lane offsets, from which the
+  // instruction offsets are taken back out, stay non-negative.
+  constexpr int kBias = 4096;
   auto rsrc = [](const uint8_t* base, int64_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), 0, (int)bytes, 0x00020000);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base) - kBias, 0, (int)(bytes + kBias), 0x00020000);
   };
   const __amdgpu_buffer_rsrc_t rac = rsrc(a_codes + a_tr0 * KT * 1024, (int64_t)Gm::at * KT * 1024);
   const __amdgpu_buffer_rsrc_t rwc = rsrc(w_codes + w_tr0 * KT * 1024, (int64_t)Gm::wt * KT * 1024);
   const __amdgpu_buffer_rsrc_t ras = rsrc(a_scales + a_tr0 * KT * 128, (int64_t)Gm::at * KT * 128);
   const __amdgpu_buffer_rsrc_t rws = rsrc(w_scales + w_tr0 * KT * 128, (int64_t)Gm::wt * KT * 128);
+  // wavefront w loads code tiles w*CPW + u (LDS: one M0 for all of them, the
+  // instruction offset u KiB, which the hardware adds to both addresses, is
+  // taken back out of the lane offset) and scale pairs w*SPW + u
   uint32_t c_off[CPW];
   bool c_a[CPW];
-  int c_dst[CPW];
 #pragma unroll
   for (int u = 0; u < CPW; ++u) {
-    const int t = wave + Gm::waves * u;
+    const int t = wave * CPW + u;
     const bool is_a = t < Gm::at;
     const int b = is_a ? t : t - Gm::at;
     const int64_t tr = min((is_a ? a_tr0 : w_tr0) + b, (is_a ? a_tiles_r : w_tiles_r) - 1) - (is_a ? a_tr0 : w_tr0);
     c_a[u] = is_a;
-    c_off[u] = (uint32_t)(tr * KT * 1024 + chunk * 16);
-    c_dst[u] = (is_a ? Gm::a_codes : Gm::w_codes) + b * 1024;
+    c_off[u] = (uint32_t)(tr * KT * 1024 + chunk * 16 + kBias - u * 1024);
   }
+  const int c_m0 = wave * CPW * 1024;
   uint32_t s_off[SPW];
   bool s_a[SPW];
-  int s_dst[SPW];
 #pragma unroll
   for (int u = 0; u < SPW; ++u) {
-    const int idx = min(wave + Gm::waves * u, Gm::scale_loads - 1);
+    const int idx = min(wave * SPW + u, Gm::scale_loads - 1);   // past the last pair: its data, into the padding
     const int t = 2 * idx + (lane >> 5);
     const bool is_a = 2 * idx < Gm::at;   // both tiles of a pair belong to one operand (at is even)
     const int b = is_a ? t : t - Gm::at;
     const int64_t tr = min((is_a ? a_tr0 : w_tr0) + b, (is_a ? a_tiles_r : w_tiles_r) - 1) - (is_a ? a_tr0 : w_tr0);
     s_a[u] = is_a;
-    s_off[u] = (uint32_t)(tr * KT * 128 + (lane & 31) * 4);
-    s_dst[u] = Gm::a_scales + idx * 256;
+    s_off[u] = (uint32_t)(tr * KT * 128 + (lane & 31) * 4 + kBias - u * 256);
   }
+  const int s_m0 = Gm::a_scales + wave * SPW * 256;
   // stage kt into ring slot `slot` (kt past the end: the last one again)
   auto issue = [&](int kt, int slot) {
     uint8_t* stage = smem + slot * Gm::bytes;
     const int ktc = kt < KTi ? kt : KTi - 1;
-#pragma unroll
-    for (int u = 0; u < CPW; ++u)
+    static_for<0, CPW>([&](auto ic) {
+      constexpr int u = decltype(ic)::value;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(c_a[u] ? rac : rwc,
-                                               (__attribute__((address_space(3))) void*)(stage + c_dst[u]), 16,
-                                               c_off[u], ktc * 1024, 0, 0);
-#pragma unroll
-    for (int u = 0; u < SPW; ++u)
+                                               (__attribute__((address_space(3))) void*)(stage + c_m0), 16,
+                                               c_off[u], ktc * 1024, u * 1024, 0);
+    });
+    static_for<0, SPW>([&](auto ic) {
+      constexpr int u = decltype(ic)::value;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(s_a[u] ? ras : rws,
-                                               (__attribute__((address_space(3))) void*)(stage + s_dst[u]), 4,
-                                               s_off[u], ktc * 128, 0, 0);
+                                               (__attribute__((address_space(3))) void*)(stage + s_m0), 4,
+                                               s_off[u], ktc * 128, u * 256, 0);
+    });
   };
 
   float16_t acc[TM][TN];
@@ -527,7 +544,7 @@ hipError_t launch_geo(const GemmArgs& a, int64_t split, hipStream_t s) {
   const int64_t KT = round_up(a.K, 64) / 64;
   // the loaders address one workgroup's row panel of an operand with 32-bit
   // buffer offsets (at most 8 code tiles of KT KiB)
-  if ((int64_t)std::max(std::max(Gm::at, Gm::wt), std::max(Gh::at, Gh::wt)) * KT * 1024 > INT32_MAX)
+  if ((int64_t)std::max(std::max(Gm::at, Gm::wt), std::max(Gh::at, Gh::wt)) * KT * 1024 + 4096 > INT32_MAX)
     return hipErrorNotSupported;
   const Panels big{(a.M + Gm::bm - 1) / Gm::bm, (split + Gm::bn - 1) / Gm::bn, 0};
   const Panels small{split < a.N ? (a.M + Gh::bm - 1) / Gh::bm : 0, (a.N - split + Gh::bn - 1) / Gh::bn, split};

@@ -112,8 +112,8 @@ def test_invalid_arguments_rejected_on_host():
                                None) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_prefill_gemm(None, fake, fake, ctypes.byref(w), 4, 0, fake, None, None, 0, fake + 8, need,
                                None) == dq.DQ_ERR_INVALID_ARG
-    # GEMM: K of 2^24 and beyond is not implemented (32-bit row-panel offsets)
-    big = 1 << 24
+    # GEMM: K of 2^23 and beyond is not implemented (32-bit row-panel offsets)
+    big = 1 << 23
     a3, w3 = _nv(4, big, fake, fake, fake), _nv(8, big, fake, fake, fake)
     assert lib.dq_prefill_gemm(ctypes.byref(a3), None, None, ctypes.byref(w3), 4, 0, fake, None, None, 0,
                                None, 0, None) == dq.DQ_ERR_UNSUPPORTED
