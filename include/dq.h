@@ -297,7 +297,8 @@ dq_status dq_decode_gemv_nvfp4(const uint16_t* x, int64_t B, const dq_nvfp4_t* W
  * dq_prefill_gemm_mxfp4: Y[m, n] = sum_k a_hat[m, k] * w_hat[n, k] with the
  *   block scales applied inside the matrix cores and fp32 accumulation;
  *   A rows = M, cols = K; W rows = N, cols = K (K = 0 gives Y = 0);
- *   out_kind DQ_OUT_F32 / DQ_OUT_BF16, Y device [M, N] row-major. */
+ *   out_kind DQ_OUT_F32 / DQ_OUT_BF16, Y device [M, N] row-major; K < 2^23
+ *   (32-bit row-panel offsets; larger K -> DQ_ERR_UNSUPPORTED). */
 dq_status dq_pack_mxfp4(const float* W, int64_t N, int64_t K, const dq_mxfp4_t* out, void* stream);
 dq_status dq_quantize_act_mxfp4(const uint16_t* X, int64_t M, int64_t K, const dq_mxfp4_t* out,
                                 void* stream);

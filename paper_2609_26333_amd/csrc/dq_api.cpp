@@ -437,6 +437,7 @@ dq_status dq_prefill_gemm_mxfp4(const dq_mxfp4_t* A, const dq_mxfp4_t* W, int ou
   st = check_mxfp4(A, "A", A->rows, W->cols);
   if (st != DQ_OK) return st;
   if (out_kind != DQ_OUT_F32 && out_kind != DQ_OUT_BF16) return fail(DQ_ERR_INVALID_ARG, "bad out_kind");
+  if (W->cols >= ((int64_t)1 << 23)) return fail(DQ_ERR_UNSUPPORTED, "K < 2^23 required (32-bit row-panel offsets)");
   if (Y == nullptr && A->rows * W->rows > 0) return fail(DQ_ERR_INVALID_ARG, "Y is NULL");
   if (!aligned(Y, 16)) return fail(DQ_ERR_INVALID_ARG, "Y must be 16-byte aligned");
   dq::MxGemmArgs a{};

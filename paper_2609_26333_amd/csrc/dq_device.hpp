@@ -1,10 +1,13 @@
-// Device helpers shared by the gfx950 kernels: operand vector types, the
-// E4M3 / E2M1 encoders used by the NVFP4 quantizers, exact fp32 division by a
-// block scale, and the tiled NVFP4 / LUT layout offsets declared in dq.h.
+// Device helpers shared by the gfx950 kernels: operand vector types, a
+// compile-time loop, the E4M3 / E2M1 encoders used by the NVFP4 quantizers,
+// exact fp32 division by a block scale, and the tiled NVFP4 / LUT layout
+// offsets declared in dq.h.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 namespace dq {
 
@@ -18,6 +21,16 @@ typedef uint32_t uint3_t __attribute__((ext_vector_type(3)));
 typedef uint32_t uint4_t __attribute__((ext_vector_type(4)));
 
 constexpr float kGlobalDivisor = 2688.0f;  // 6 * 448: E2M1 max times E4M3 max
+
+// f(integral_constant<int, U>) for U = B .. E - 1: unrolled loops whose
+// index must be a compile-time constant (instruction offsets)
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
 
 // ---------------------------------------------------------------- layouts
 // NVFP4 "32x64 tiles" (see dq.h).

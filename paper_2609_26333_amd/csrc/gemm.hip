@@ -81,15 +81,6 @@ struct Geo {
   static_assert(stages >= 4 && (stages - 1) * loads_per_wave <= 63, "LDS ring of four to six stages");
 };
 
-// f(integral_constant<int, U>) for U = B .. E - 1 (compile-time indices)
-template <int B, int E, class F>
-__device__ __forceinline__ void static_for(F&& f) {
-  if constexpr (B < E) {
-    f(std::integral_constant<int, B>{});
-    static_for<B + 1, E>(f);
-  }
-}
-
 // 8 E2M1 codes (one dword) times an fp16 block scale -> 8 exact fp16 values.
 __device__ inline half8_t dequant8(uint32_t w, half2_t s) {
   half2_t p0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 0) * s;

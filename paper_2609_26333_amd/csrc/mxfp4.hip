@@ -38,6 +38,8 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <climits>
+#include <type_traits>
 
 #include "dq_device.hpp"
 #include "dq_internal.hpp"
@@ -203,41 +205,62 @@ __device__ __forceinline__ void mx_gemm_tile(int64_t blk, const MxPanels& P, con
   const int64_t n0 = n_off + bn * Gm::bn + wn * 32 * TN;
   const int KTi = (int)KT;
 
-  // Direct loads: code tiles t = wave + waves*u (A tiles first, then W);
-  // scale instruction `wave` covers one 4-tile group (256 bytes).  Tiles past
-  // the end of an operand read its last row tile (in bounds): they only feed
-  // output rows / columns that are never stored.  K steps past the end
-  // reload the last one into a slot that is no longer read, so that every
-  // step issues the same loads (no branches in the main loop).
+  // Direct loads: wavefront w loads code tiles w*CPW + u (A tiles first,
+  // then W, contiguous in LDS) with one M0 and the LDS placement in the
+  // instruction offset (which the hardware adds to both addresses; the lane
+  // offsets subtract it back out); scale instruction `wave` covers one 4-tile
+  // group (256 bytes), waves past the last group repeating it.  Each operand
+  // row panel is one buffer resource (per load a fixed lane offset, per K
+  // step one scalar offset), based kBias bytes low so that the lane offsets
+  // stay non-negative.  Tiles past the end of an operand read its last row
+  // tile (in bounds): they only feed output rows / columns that are never
+  // stored.  K steps past the end reload the last one into a slot that is no
+  // longer read, so that every step issues the same loads (no branches in
+  // the main loop).
   const int chunk = 2 * (lane & 31) + (lane >> 5);
   constexpr int CPW = Gm::code_loads / Gm::waves;
-  const uint8_t* c_src[CPW];
-  int c_dst[CPW];
+  constexpr int kBias = 4096;
+  static_assert(CPW * 1024 <= kBias, "instruction offsets within the bias");
+  auto rsrc = [](const uint8_t* base, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base) - kBias, 0, (int)(bytes + kBias), 0x00020000);
+  };
+  const __amdgpu_buffer_rsrc_t rac = rsrc(a_codes + a_tr0 * KT * 1024, (int64_t)Gm::at * KT * 1024);
+  const __amdgpu_buffer_rsrc_t rwc = rsrc(w_codes + w_tr0 * KT * 1024, (int64_t)Gm::wt * KT * 1024);
+  const __amdgpu_buffer_rsrc_t ras = rsrc(a_scales + (a_tr0 / 4) * KT * 256, (int64_t)(Gm::at / 4) * KT * 256);
+  const __amdgpu_buffer_rsrc_t rws = rsrc(w_scales + (w_tr0 / 4) * KT * 256, (int64_t)(Gm::wt / 4) * KT * 256);
+  uint32_t c_off[CPW];
+  bool c_a[CPW];
 #pragma unroll
   for (int u = 0; u < CPW; ++u) {
-    const int t = wave + Gm::waves * u;
+    const int t = wave * CPW + u;
     const bool is_a = t < Gm::at;
     const int b = is_a ? t : t - Gm::at;
-    const int64_t tr = min((is_a ? a_tr0 : w_tr0) + b, (is_a ? a_tiles_r : w_tiles_r) - 1);
-    c_src[u] = (is_a ? a_codes : w_codes) + tr * KT * 1024 + chunk * 16;
-    c_dst[u] = (is_a ? Gm::a_codes : Gm::w_codes) + b * 1024;
+    const int64_t tr0 = is_a ? a_tr0 : w_tr0;
+    const int64_t tr = min(tr0 + b, (is_a ? a_tiles_r : w_tiles_r) - 1) - tr0;
+    c_a[u] = is_a;
+    c_off[u] = (uint32_t)(tr * KT * 1024 + chunk * 16 + kBias - u * 1024);
   }
+  const int c_m0 = wave * CPW * 1024;
   const int si = min(wave, Gm::scale_loads - 1);   // waves past the last scale group repeat it
   const bool s_is_a = si < Gm::at / 4;
   const int64_t a_groups = (a_tiles_r + 3) / 4, w_groups = (w_tiles_r + 3) / 4;
-  const int64_t sg = min((s_is_a ? a_tr0 : w_tr0) / 4 + (s_is_a ? si : si - Gm::at / 4),
-                         (s_is_a ? a_groups : w_groups) - 1);
-  const uint8_t* s_src = (s_is_a ? a_scales : w_scales) + sg * KT * 256 + lane * 4;
+  const int64_t g0 = (s_is_a ? a_tr0 : w_tr0) / 4;
+  const int64_t sg = min(g0 + (s_is_a ? si : si - Gm::at / 4), (s_is_a ? a_groups : w_groups) - 1) - g0;
+  const uint32_t s_off = (uint32_t)(sg * KT * 256 + lane * 4 + kBias);
   const int s_dst = Gm::a_scales + si * 256;
-  auto issue = [&](int kt) {
-    uint8_t* stage = smem + (kt % S) * Gm::bytes;
+  // stage kt into the ring slot at byte offset `off` (kt past the end: the last one again)
+  auto issue = [&](int kt, int off) {
+    uint8_t* stage = smem + off;
     const int ktc = kt < KTi ? kt : KTi - 1;
-#pragma unroll
-    for (int u = 0; u < CPW; ++u)
-      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(c_src[u] + (size_t)ktc * 1024),
-                                       reinterpret_cast<void*>(stage + c_dst[u]), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(s_src + (size_t)ktc * 256),
-                                     reinterpret_cast<void*>(stage + s_dst), 4, 0, 0);
+    static_for<0, CPW>([&](auto ic) {
+      constexpr int u = decltype(ic)::value;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(c_a[u] ? rac : rwc,
+                                               (__attribute__((address_space(3))) void*)(stage + c_m0), 16,
+                                               c_off[u], ktc * 1024, u * 1024, 0);
+    });
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(s_is_a ? ras : rws,
+                                             (__attribute__((address_space(3))) void*)(stage + s_dst), 4, s_off,
+                                             ktc * 256, 0, 0);
   };
 
   float16_t acc[TM][TN];
@@ -295,7 +318,7 @@ __device__ __forceinline__ void mx_gemm_tile(int64_t blk, const MxPanels& P, con
   if (KTi > 0) {
     // prologue: stages 0 .. S-1 in flight, stage 0 landed everywhere
 #pragma unroll
-    for (int st = 0; st < S; ++st) issue(st);
+    for (int st = 0; st < S; ++st) issue(st, st * Gm::bytes);
     mx_wait_vm<(S - 1) * L>();
     mx_barrier();
     Ops o0, o1;
@@ -307,7 +330,9 @@ __device__ __forceinline__ void mx_gemm_tile(int64_t blk, const MxPanels& P, con
     // sched_barriers keep this order; the empty asm statements pin the
     // accumulators at the end of the step (otherwise the compiler sinks the
     // MFMAs, pure register operations, into the next step).
-    auto step = [&](int kt, Ops& cur, Ops& nxt) {
+    // off: byte offset of stage kt's ring slot (refilled with stage kt+S),
+    // noff: that of stage kt+1
+    auto step = [&](int kt, Ops& cur, Ops& nxt, int off, int noff) {
       __builtin_amdgcn_s_waitcnt((0x3F & 0xF) | (0x7 << 4) | (0x0 << 8) | ((0x3F >> 4) << 14));   // lgkmcnt(0)
       mfma_one(cur, 0);
       mfma_one(cur, 1);
@@ -316,8 +341,8 @@ __device__ __forceinline__ void mx_gemm_tile(int64_t blk, const MxPanels& P, con
       mx_barrier();
       mfma_one(cur, 2);
       __builtin_amdgcn_sched_barrier(0);
-      issue(kt + S);
-      const uint8_t* stg = smem + ((kt + 1) % S) * Gm::bytes;
+      issue(kt + S, off);
+      const uint8_t* stg = smem + noff;
 #pragma unroll
       for (int q = 3; q < kSlots; ++q) {
         __builtin_amdgcn_sched_barrier(0);
@@ -334,19 +359,26 @@ __device__ __forceinline__ void mx_gemm_tile(int64_t blk, const MxPanels& P, con
     // Full steps 0 .. KT-2 alternate o0 -> o1 and o1 -> o0; the first one is
     // peeled when their number is odd, so that the last step always consumes o0.
     const int full = KTi - 1;
-    int kt = 0;
+    int kt = 0, off = 0, noff = Gm::bytes;
+    auto adv = [&](int o) { return o + Gm::bytes == S * Gm::bytes ? 0 : o + Gm::bytes; };
     if (full & 1) {
 #pragma unroll
       for (int r = 0; r < kReads; ++r) read_one(smem, o1, r);
-      step(0, o1, o0);
+      step(0, o1, o0, off, noff);
       kt = 1;
+      off = noff;
+      noff = adv(noff);
     } else {
 #pragma unroll
       for (int r = 0; r < kReads; ++r) read_one(smem, o0, r);
     }
     for (; kt < full; kt += 2) {
-      step(kt, o0, o1);
-      step(kt + 1, o1, o0);
+      step(kt, o0, o1, off, noff);
+      off = noff;
+      noff = adv(noff);
+      step(kt + 1, o1, o0, off, noff);
+      off = noff;
+      noff = adv(noff);
     }
     __builtin_amdgcn_s_waitcnt((0x3F & 0xF) | (0x7 << 4) | (0x0 << 8) | ((0x3F >> 4) << 14));   // lgkmcnt(0)
 #pragma unroll
@@ -457,6 +489,10 @@ hipError_t launch_mx_geo(const MxGemmArgs& a, int64_t split, hipStream_t s) {
   const int64_t a_tiles_r = round_up(a.M, 32) / 32;
   const int64_t w_tiles_r = round_up(a.N, 32) / 32;
   const int64_t KT = round_up(a.K, 64) / 64;
+  // the loaders address one workgroup's row panel of an operand with 32-bit
+  // buffer offsets (at most 8 code tiles of KT KiB, plus the bias)
+  if ((int64_t)std::max(std::max(Gf::at, Gf::wt), std::max(Gh::at, Gh::wt)) * KT * 1024 + 4096 > INT32_MAX)
+    return hipErrorNotSupported;
   const MxPanels full{(a.M + Gf::bm - 1) / Gf::bm, (split + Gf::bn - 1) / Gf::bn, 0};
   const MxPanels half{split < a.N ? (a.M + Gh::bm - 1) / Gh::bm : 0, (a.N - split + Gh::bn - 1) / Gh::bn, split};
   const int64_t blocks = full.tiles_m * full.tiles_n + half.tiles_m * half.tiles_n;

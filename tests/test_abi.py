@@ -77,6 +77,9 @@ def test_mxfp4_arguments_rejected_on_host():
     assert lib.dq_prefill_gemm_mxfp4(P(mx(4, 64)), P(mx(8, 64)), dq.OUT_NVFP4, fake, None) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_prefill_gemm_mxfp4(P(mx(4, 64)), P(mx(8, 64)), 0, None, None) == dq.DQ_ERR_INVALID_ARG
     assert lib.dq_prefill_gemm_mxfp4(None, P(mx(8, 64)), 0, fake, None) == dq.DQ_ERR_INVALID_ARG
+    # GEMM: K of 2^23 and beyond is not implemented (32-bit row-panel offsets)
+    big = 1 << 23
+    assert lib.dq_prefill_gemm_mxfp4(P(mx(4, big)), P(mx(8, big)), 0, fake, None) == dq.DQ_ERR_UNSUPPORTED
 
 
 def _nv(rows, cols, codes=16, scales=16, G=16):
