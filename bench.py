@@ -52,7 +52,7 @@ PEAK_FP16_TFLOPS = 2500.0      # dense fp16/bf16 MFMA, MI355X
 PEAK_FP4_TFLOPS = 10100.0      # dense fp4 MFMA, MI355X
 PEAK_HBM_GBS = 8000.0
 # sources that decide the GEMM's kernels and launches
-GEMM_SOURCES = [os.path.join(ROOT, "paper_2609_26333_amd", "csrc", f) for f in ("gemm.hip", "dq_internal.hpp")]
+GEMM_SOURCES = [os.path.join(ROOT, "paper_2609_26333_amd", "csrc", f) for f in ("gemm.hip", "dq_internal.hpp", "dq_device.hpp")]
 GEMM_COUNTERS = os.path.join(ROOT, "profiles", "nvfp4_gemm_27b_down_m32768_counters.md")
 COPY_BYTES = 256 << 20
 SWEEP = ((3, 1), (3, 8), (3, 16), (2, 1), (2, 8), (2, 16))
