@@ -55,6 +55,17 @@ PEAK_HBM_GBS = 8000.0
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2609_26333_amd", "csrc", f) for f in ("gemm.hip", "dq_internal.hpp", "dq_device.hpp")]
 GEMM_COUNTERS = os.path.join(ROOT, "profiles", "nvfp4_gemm_27b_down_m32768_counters.md")
 COPY_BYTES = 256 << 20
+# The paper's end-to-end figure for this method, quoted as context only: a
+# whole-model time to first token on other hardware, not a kernel rate and
+# not comparable with the numbers measured here (paper Sec. 1 and Sec. 3.2,
+# hardware as stated in Sec. 3.1).
+PAPER_CONTEXT = {
+    "what": "time to first token, Qwen3.8-27B at an 8K-token prompt, llama.cpp",
+    "weight_only_iq1s_s": 12.27, "odp_nvfp4_prefiller_s": 6.90, "speedup": 1.78,
+    "speedup_range_4k_to_32k": [1.38, 1.78],
+    "hardware": "one NVIDIA GB10 (DGX Spark)",
+    "note": "context only; no absolute TFLOP/s or GB/s is published for this path",
+}
 SWEEP = ((3, 1), (3, 8), (3, 16), (2, 1), (2, 8), (2, 16))
 
 # Clock sampler: a separate process, started before this one touches the GPU,
@@ -439,6 +450,7 @@ def run(args, clk_path):
         "roofline_decode": {"bound": "hbm", "kernel": "LUT3 batch-1 token: 256 dq_decode_gemv launches",
                             "achieved": decode["lut3_b1"]["GB/s"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
                             "frac": decode["lut3_b1"]["frac_hbm"]},
+        "paper_context": PAPER_CONTEXT,
     }
     if not args.no_extras:
         out["decode_differencing"] = decode_differencing(dq, torch, lib, s, stacks[3], xs[1], ys[1], cfg,
