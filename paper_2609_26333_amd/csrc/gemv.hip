@@ -604,13 +604,25 @@ void lut_gemv_persist_kernel(const uint16_t* __restrict__ x, int B, int64_t K, c
   // for every load at the top of each cycle), then the remaining slots
   const int full = total / RING * RING;
   const int q1 = total / 4, q2 = total / 2, q3 = (3 * total) / 4;
-  for (int f0 = 0; f0 < full; f0 += RING) {
-    if (f0 >= q3)
-      __builtin_amdgcn_s_setprio(0);
-    else if (f0 >= q2)
-      __builtin_amdgcn_s_setprio(1);
-    else if (f0 >= q1)
-      __builtin_amdgcn_s_setprio(2);
+  // one loop per priority level (s_setprio takes an immediate), so that the
+  // cycles carry no branches for it
+  int f0 = 0;
+  for (; f0 < full && f0 < q1; f0 += RING) {
+#pragma unroll
+    for (int r = 0; r < RING; ++r) slot(r);
+  }
+  __builtin_amdgcn_s_setprio(2);
+  for (; f0 < full && f0 < q2; f0 += RING) {
+#pragma unroll
+    for (int r = 0; r < RING; ++r) slot(r);
+  }
+  __builtin_amdgcn_s_setprio(1);
+  for (; f0 < full && f0 < q3; f0 += RING) {
+#pragma unroll
+    for (int r = 0; r < RING; ++r) slot(r);
+  }
+  __builtin_amdgcn_s_setprio(0);
+  for (; f0 < full; f0 += RING) {
 #pragma unroll
     for (int r = 0; r < RING; ++r) slot(r);
   }
@@ -902,13 +914,25 @@ void lut_gemv_split_kernel(const uint16_t* __restrict__ x, int64_t K, int B, con
   // batch-1 kernel); wave priority falls with progress
   const int full = total / RING * RING;
   const int q1 = total / 4, q2 = total / 2, q3 = (3 * total) / 4;
-  for (int f0 = 0; f0 < full; f0 += RING) {
-    if (f0 >= q3)
-      __builtin_amdgcn_s_setprio(0);
-    else if (f0 >= q2)
-      __builtin_amdgcn_s_setprio(1);
-    else if (f0 >= q1)
-      __builtin_amdgcn_s_setprio(2);
+  // one loop per priority level (s_setprio takes an immediate), so that the
+  // cycles carry no branches for it
+  int f0 = 0;
+  for (; f0 < full && f0 < q1; f0 += RING) {
+#pragma unroll
+    for (int r = 0; r < RING; ++r) slot(r);
+  }
+  __builtin_amdgcn_s_setprio(2);
+  for (; f0 < full && f0 < q2; f0 += RING) {
+#pragma unroll
+    for (int r = 0; r < RING; ++r) slot(r);
+  }
+  __builtin_amdgcn_s_setprio(1);
+  for (; f0 < full && f0 < q3; f0 += RING) {
+#pragma unroll
+    for (int r = 0; r < RING; ++r) slot(r);
+  }
+  __builtin_amdgcn_s_setprio(0);
+  for (; f0 < full; f0 += RING) {
 #pragma unroll
     for (int r = 0; r < RING; ++r) slot(r);
   }
