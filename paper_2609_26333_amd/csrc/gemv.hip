@@ -585,7 +585,7 @@ void lut_gemv_persist_kernel(const uint16_t* __restrict__ x, int B, int64_t K, c
         if (MODE == 1) af = scale_half8(af, st < 2 ? s_lo : s_hi);
         pacc[st] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf[st], pacc[st], 0, 0, 0);
       }
-      if (++s == CPW) {
+      if (__builtin_expect(++s == CPW, 0)) {   // end of a round: rare
         s = 0;
         if (rd < nr) {   // end of round rd: park the partial sums
           float4_t acc;
@@ -880,7 +880,7 @@ void lut_gemv_split_kernel(const uint16_t* __restrict__ x, int64_t K, int B, con
         if (MODE == 1) af = scale_half8(af, st < 2 ? s_lo : s_hi);
         pacc[st] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bf[st], pacc[st], 0, 0, 0);
       }
-      if (++u == nc) {   // end of tile ti_: lane (q, j) stores rows 4q..4q+3 of batch row j
+      if (__builtin_expect(++u == nc, 0)) {   // end of tile ti_: lane (q, j) stores rows 4q..4q+3 of batch row j
         u = 0;
         float4_t acc;
 #pragma unroll
