@@ -134,14 +134,6 @@ enum { kOutF32 = 0, kOutBF16 = 1, kOutNvfp4 = 2 };
 // silu(g) * u in fp32 (SwiGLU, the MLP non-linearity between gate/up and down)
 __device__ inline float swiglu(float g, float u) { return g / (1.0f + expf(-g)) * u; }
 
-// One E2M1 code (low nibble) of v for the block scale S != 0: the same
-// arithmetic as the activation quantizer (correctly rounded v / S, hardware
-// round-to-nearest-even with saturation, +0 for magnitude zero).
-__device__ inline uint32_t e2m1_code(float v, float S) {
-  const float rcp = 1.0f / S;
-  return fp4_canonical_zero(cvt_pk_fp4<0>(0u, div_by_scale(v, S, rcp), 0.0f)) & 0xFu;
-}
-
 // Workgroup tiles of one geometry: tiles_m x tiles_n tiles over the output
 // columns from n_off on.
 struct Panels {
@@ -487,13 +479,18 @@ __device__ __forceinline__ void gemm_tile(
           a = fmaxf(a, __shfl_xor(a, 32, 64));
           const uint32_t c = e4m3_encode_rne_sat(a / den);
           const float Sc = e4m3_decode(c) * Go;
-          uint32_t P0 = 0u, P1 = 0u;
+          // the 8 codes as one dword (value e in nibble e): the activation
+          // quantizer's arithmetic, two conversions per instruction
+          const float rcp = 1.0f / Sc;   // Sc == 0: the codes are forced to 0 below
+          float yq[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const uint32_t code = Sc == 0.0f ? 0u : e2m1_code(v[e], Sc);
-            if (e < 4) P0 |= code << (4 * e);
-            else P1 |= code << (4 * (e - 4));
-          }
+          for (int e = 0; e < 8; ++e) yq[e] = div_by_scale(v[e], Sc, rcp);
+          uint32_t cw = cvt_pk_fp4<0>(0u, yq[0], yq[1]);
+          cw = cvt_pk_fp4<1>(cw, yq[2], yq[3]);
+          cw = cvt_pk_fp4<2>(cw, yq[4], yq[5]);
+          cw = cvt_pk_fp4<3>(cw, yq[6], yq[7]);
+          cw = Sc == 0.0f ? 0u : fp4_canonical_zero(cw);
+          const uint32_t P0 = cw & 0xFFFFu, P1 = cw >> 16;
           // dword 0 = columns cbase..+7 (h = 0's P0, h = 1's P0); dword 1 =
           // columns cbase+8..+15 (h = 0's P1, h = 1's P1)
           const uint32_t recv = (uint32_t)__shfl_xor((int)(h == 0 ? P1 : P0), 32, 64);
