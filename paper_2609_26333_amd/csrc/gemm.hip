@@ -525,7 +525,7 @@ __global__ __launch_bounds__(Gm::threads, Gm::occ) void nvfp4_gemm_kernel(
 // One launch: output columns 0 .. split-1 in Gm tiles, split .. N-1 in Gh
 // tiles (split a multiple of Gm::bn and of 128, so that an NVFP4 output tile
 // of the SwiGLU half-width result never straddles the two; or N).
-template <class Gm, class Gh>
+template <class Gm, class Gh, bool kBf16Only = false>
 hipError_t launch_geo(const GemmArgs& a, int64_t split, hipStream_t s) {
   const int64_t a_tiles_r = round_up(a.M, 32) / 32;
   const int64_t w_tiles_r = round_up(a.N, 32) / 32;
@@ -553,11 +553,16 @@ hipError_t launch_geo(const GemmArgs& a, int64_t split, hipStream_t s) {
   }
   typedef void (*kern_t)(const uint8_t*, const uint8_t*, const float*, const uint8_t*, const uint8_t*, const float*,
                          int64_t, int64_t, int64_t, int64_t, int64_t, GemmOut, Panels, Panels);
-  static const kern_t kerns[3][2] = {
-      {nvfp4_gemm_kernel<Gm, Gh, kOutF32, false>, nvfp4_gemm_kernel<Gm, Gh, kOutF32, true>},
-      {nvfp4_gemm_kernel<Gm, Gh, kOutBF16, false>, nvfp4_gemm_kernel<Gm, Gh, kOutBF16, true>},
-      {nvfp4_gemm_kernel<Gm, Gh, kOutNvfp4, false>, nvfp4_gemm_kernel<Gm, Gh, kOutNvfp4, true>}};
-  const kern_t kern = kerns[a.out_kind][sw ? 1 : 0];
+  kern_t kern;
+  if constexpr (kBf16Only) {
+    kern = nvfp4_gemm_kernel<Gm, Gh, kOutBF16, false>;
+  } else {
+    static const kern_t kerns[3][2] = {
+        {nvfp4_gemm_kernel<Gm, Gh, kOutF32, false>, nvfp4_gemm_kernel<Gm, Gh, kOutF32, true>},
+        {nvfp4_gemm_kernel<Gm, Gh, kOutBF16, false>, nvfp4_gemm_kernel<Gm, Gh, kOutBF16, true>},
+        {nvfp4_gemm_kernel<Gm, Gh, kOutNvfp4, false>, nvfp4_gemm_kernel<Gm, Gh, kOutNvfp4, true>}};
+    kern = kerns[a.out_kind][sw ? 1 : 0];
+  }
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
@@ -577,19 +582,42 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(publish_scale_kernel, dim3(1), dim3(1), 0, s, a.G_out, a.Yq.G);
     return hipGetLastError();
   }
-  // 256x128 workgroup tiles as 2x2 wavefronts of 128x64, two workgroups per
-  // compute unit (two wavefronts per SIMD): one workgroup's dequantization
-  // and barrier waits overlap the other's MFMAs, and a workgroup's output
-  // stores overlap the other's main loop.  128x128 tiles (2x2 wavefronts of
-  // 64x64) dequantize a third more operand elements per MFMA, so they only
-  // take the columns of a last round that would leave most slots empty (at
-  // most a quarter full), or the whole grid when it is under one round.
-  // Measured on the paper's linears: the 27B o-projection (a quarter-full
-  // last round) 10 % faster, shapes with a half-full last round unchanged
-  // or 1-2 % slower, so those keep 256x128 tiles.
+  // bf16 output without SwiGLU on grids of at least two full rounds of
+  // 256x256 tiles: one workgroup of four 128x128 wavefronts per compute unit
+  // (one wavefront per SIMD, 256 accumulator registers).  A wavefront
+  // dequantizes a quarter fewer operand elements per MFMA than a 128x64 one;
+  // on such grids that outweighs the lost overlap between two workgroups
+  // (27B down-projection at M = 32768 4-5 % faster, M = 8192 3 %, the 8B
+  // down-projection at M = 8192 6 %, the 27B gate/up shape at M = 4096 2 %).
+  // The NVFP4 and SwiGLU epilogues are longer and lose more than that when no
+  // second workgroup runs its main loop meanwhile (2-7 % slower at
+  // 4096 x 34816 x 5120).  A partial last round of at most half the compute
+  // units takes the trailing columns as 256x128 tiles, one per compute unit.
+  const int cus = num_cus();
+  if (a.out_kind == kOutBF16 && (a.flags & 1) == 0) {
+    using Gb = Geo<4, 4, 2, 2, 1>;
+    using Gbh = Geo<4, 2, 2, 2, 1>;
+    const int64_t tm = (a.M + Gb::bm - 1) / Gb::bm, panels = (a.N + Gb::bn - 1) / Gb::bn;
+    const int64_t tiles = tm * panels, rounds = tiles / cus, rest = tiles % cus;
+    if (rounds >= 2) {
+      const int64_t split = rest > 0 && 2 * rest <= cus ? rounds * cus / tm * Gb::bn : a.N;
+      return launch_geo<Gb, Gbh, true>(a, split, s);
+    }
+  }
+  // Otherwise 256x128 workgroup tiles as 2x2 wavefronts of 128x64, two
+  // workgroups per compute unit (two wavefronts per SIMD): one workgroup's
+  // dequantization and barrier waits overlap the other's MFMAs, and a
+  // workgroup's output stores overlap the other's main loop (on grids of one
+  // or two rounds 9-17 % faster than the 256x256 tiles).  128x128 tiles (2x2
+  // wavefronts of 64x64) dequantize a third more operand elements per MFMA,
+  // so they only take the columns of a last round that would leave most
+  // slots empty (at most a quarter full), or the whole grid when it is under
+  // one round.  Measured on the paper's linears: the 27B o-projection (a
+  // quarter-full last round) 10 % faster, shapes with a half-full last round
+  // unchanged or 1-2 % slower, so those keep 256x128 tiles.
   using Gm = Geo<4, 2, 2, 2, 2>;
   using Gh = Geo<2, 2, 2, 2, 2>;
-  const int64_t slots = (int64_t)num_cus() * Gm::occ;
+  const int64_t slots = (int64_t)cus * Gm::occ;
   const int64_t tm = (a.M + Gm::bm - 1) / Gm::bm, panels = (a.N + Gm::bn - 1) / Gm::bn;
   const int64_t tiles = tm * panels, rounds = tiles / slots, rest = tiles % slots;
   int64_t split = a.N;

@@ -267,6 +267,45 @@ def test_gemm_tile_geometries_agree(M, N, K, out):
         PB.assert_within(y, ref, bound, "geometries bf16", bf16=True)
 
 
+@pytest.mark.parametrize("M,N,K", [(4096, 8192, 128), (4000, 8320, 192), (4096, 16640, 64)])
+def test_gemm_wide_tile_geometry_agrees(M, N, K):
+    """bf16 outputs of grids of at least two rounds of 256x256 tiles run as
+    one workgroup of four 128x128 wavefronts per compute unit (with a partial
+    last round of 256x128 tiles in the trailing columns when N is not a whole
+    number of rounds); 32-row slices launch the small-tile geometry.  Every
+    output is accumulated over K in the same order, so the slices equal the
+    full call bit for bit (ragged rows and edge columns included), and
+    sampled rows of the full call match the oracle."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    assert ((M + 255) // 256) * ((N + 255) // 256) >= 2 * cus, "shape must take the 256x256 geometry"
+    say("wide geometry", M, N, K)
+    xb = synth.random_bf16(93, (M, K), outlier_frac=0.01, outlier_factor=20)
+    w = synth.random_f32(94, (N, K), 0.02)
+    G_x = nvfp4.global_scale(nvfp4.amax(formats.f32_from_bf16_bits(xb)))
+    Gd = dev(np.array([G_x], np.float32))
+    W = dq.dq_pack_nvfp4(dev(w))
+
+    def run(rows):
+        A = dq.dq_quantize_act_nvfp4(bf16_dev(xb[rows]), G_static=Gd)
+        Y = dq.dq_prefill_gemm(W, A=A, out_kind=dq.OUT_BF16)
+        return host(Y.view(torch.int16))
+
+    full = run(np.arange(M))
+    for r0 in (0, 1056, M - 32):
+        rows = np.arange(r0, r0 + 32)
+        assert np.array_equal(run(rows), full[rows]), f"rows {r0}..{r0 + 31} differ"
+    rows = np.sort(np.random.default_rng(95).choice(M, 6, replace=False))
+    qa, ca, _ = nvfp4.quantize_bf16_activations(xb[rows], G_x)
+    qw, cw, Gw = nvfp4.quantize_dynamic(w)
+    ref = linalg.nvfp4_gemm(qa, ca, G_x, qw, cw, Gw)
+    y = formats.f64_from_bf16_bits(full[rows].view(np.uint16))
+    err = linalg.rel_fro(y, formats.bf16_rne_from_f64(ref))
+    say("  sampled rel_fro", err)
+    assert err <= TOL
+    bound = PB.fp32_sum_bound(PB.abs_products(nvfp4.dequantize(qa, ca, G_x), nvfp4.dequantize(qw, cw, Gw)), K)
+    PB.assert_within(y, ref, bound, "wide geometry", bf16=True)
+
+
 FUSED_SHAPES = [(128, 512, 512), (300, 520, 1024), (1, 16, 64), (0, 32, 64)]
 
 
