@@ -17,9 +17,11 @@ Weights 0.02 N(0,1) times a log-normal row scale; activations N(0,1) with
 0.5 % outlier channels x30 (seeded synthetic tensors, resident in HBM).
 
 One step = prefill quantization + GEMM + the six decode tokens.  The run
-does `warmup` steps, then times `steps` steps between two HIP events on the
-launch stream (`ms_per_step`); HIP events between the phases of every timed
-step give each phase's average duration.  `value` is the prefill linear's
+does `warmup` steps (phases interleaved), then times `steps` steps between
+two HIP events on the launch stream (`ms_per_step`), the steps' prefill
+passes first and then their decode tokens, so that each phase runs under its
+own sustained load; HIP events around every phase of every timed step give
+each phase's average duration.  `value` is the prefill linear's
 throughput 2*M*N*K / (quantization + GEMM); `roofline` is the GEMM kernel
 against the dense FP4 peak (its fp16-MFMA fraction alongside), and
 `roofline_decode` the LUT3 batch-1 token against HBM.  Outside the timed
@@ -93,7 +95,7 @@ def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=10)
-    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-extras", action="store_true", help="skip the measurements outside the timed steps")
     p.add_argument("--no-sclk", action="store_true")
@@ -376,31 +378,49 @@ def run(args, clk_path):
     torch.cuda.synchronize()
 
     # ---------------------------------------------------------------- timed steps
-    n_ph = 2 + len(SWEEP)
-
-    def step(marks):
-        marks[0].record(s)
+    # The timed region runs the K steps' prefill passes (quantization + GEMM)
+    # back to back, then their decode tokens: each phase at the clock the
+    # chip holds under that phase's own sustained load, as on a prefill
+    # engine and a decode engine of disaggregated serving.  The warm-up steps
+    # interleave the phases (quantization, GEMM, then the six tokens); their
+    # GEMM durations are reported separately (after ~25 ms of HBM-bound
+    # decode kernels the power management holds a lower clock for the next
+    # several milliseconds).
+    def prefill_pass(pm):
+        pm[0].record(s)
         quant()
-        marks[1].record(s)
+        pm[1].record(s)
         gemm()
-        marks[2].record(s)
+        pm[2].record(s)
+
+    def decode_pass(dm):
+        dm[0].record(s)
         for j, key in enumerate(SWEEP):
             graphs[key].replay()
-            marks[3 + j].record(s)
+            dm[1 + j].record(s)
 
-    for _ in range(args.warmup):
-        step([ev() for _ in range(n_ph + 1)])
+    warm_pm = [[ev() for _ in range(3)] for _ in range(args.warmup)]
+    for w in range(args.warmup):
+        prefill_pass(warm_pm[w])
+        decode_pass([ev() for _ in range(len(SWEEP) + 1)])
     torch.cuda.synchronize()
-    marks = [[ev() for _ in range(n_ph + 1)] for _ in range(args.steps)]
+    gemm_interleaved_ms = [m[1].elapsed_time(m[2]) for m in warm_pm[1:]]   # the first warm-up step is cold
+    pms = [[ev() for _ in range(3)] for _ in range(args.steps)]
+    dms = [[ev() for _ in range(len(SWEEP) + 1)] for _ in range(args.steps)]
     t_start, t_end = ev(), ev()
     t_start.record(s)
     for i in range(args.steps):
-        step(marks[i])
+        prefill_pass(pms[i])
+    for i in range(args.steps):
+        decode_pass(dms[i])
     t_end.record(s)
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
-    ph = [sum(m[j].elapsed_time(m[j + 1]) for m in marks) / args.steps for j in range(n_ph)]   # ms
-    ph_med = [float(np.median([m[j].elapsed_time(m[j + 1]) for m in marks])) for j in range(n_ph)]   # ms
+    spans = [[m[0].elapsed_time(m[1]), m[1].elapsed_time(m[2])] + [d[j].elapsed_time(d[j + 1]) for j in range(len(SWEEP))]
+             for m, d in zip(pms, dms)]   # ms, per step: quantization, GEMM, the six tokens
+    n_ph = 2 + len(SWEEP)
+    ph = [sum(sp_[j] for sp_ in spans) / args.steps for j in range(n_ph)]
+    ph_med = [float(np.median([sp_[j] for sp_ in spans])) for j in range(n_ph)]
     t_quant, t_gemm = ph[0] * 1e-3, ph[1] * 1e-3
 
     flops = 2.0 * M * N * K
@@ -434,7 +454,12 @@ def run(args, clk_path):
                     "gemm_us": t_gemm * 1e6, "gemm_TFLOP/s": gemm_tflops,
                     "frac_fp4_peak": gemm_tflops / PEAK_FP4_TFLOPS,
                     "frac_fp16_mfma_peak": gemm_tflops / PEAK_FP16_TFLOPS,
-                    "linear_TFLOP/s_incl_quant": prefill_tflops},
+                    "linear_TFLOP/s_incl_quant": prefill_tflops,
+                    "gemm_us_interleaved": (float(np.median(gemm_interleaved_ms)) * 1e3 if gemm_interleaved_ms
+                                            else None),
+                    "order": ("timed: the steps' prefill passes back to back, then their decode tokens; "
+                              "gemm_us_interleaved: median GEMM of the warm-up steps after the first, each "
+                              "right after the previous step's six decode tokens")},
         "decode": decode,
         "roofline": {"bound": "mfma", "kernel": "nvfp4_gemm_kernel (one launch per dq_prefill_gemm call)",
                      "achieved": gemm_tflops, "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s",
