@@ -90,6 +90,17 @@ __device__ inline half8_t dequant8(uint32_t w, half2_t s) {
   return half8_t{p0[0], p0[1], p1[0], p1[1], p2[0], p2[1], p3[0], p3[1]};
 }
 
+// Half of dequant8: values 4*HF .. 4*HF+3 of the dword into v
+template <int HF>
+__device__ inline void dequant4(uint32_t w, half2_t s, half8_t& v) {
+  const half2_t p0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 2 * HF) * s;
+  const half2_t p1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 2 * HF + 1) * s;
+  v[4 * HF] = p0[0];
+  v[4 * HF + 1] = p0[1];
+  v[4 * HF + 2] = p1[0];
+  v[4 * HF + 3] = p1[1];
+}
+
 // One of the two E4M3 scale bytes in sc (byte `hi`) -> fp16 broadcast pair
 __device__ inline half2_t scale_pair(uint32_t sc, int hi) {
   const half2_t s = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sc, 1.0f, false);
@@ -268,6 +279,22 @@ __device__ __forceinline__ void gemm_tile(
     if (u < TM) D.a[u] = dequant8(R.a[u][s], scale_pair(R.sa[u], s >> 1));
     else D.w[u - TM] = dequant8(R.w[u - TM][s], scale_pair(R.sw[u - TM], s >> 1));
   };
+  // the same in two halves, issued after different MFMAs (tile u's scale
+  // pair kept in sp[u] between them)
+  half2_t sp[kTiles];
+  auto dequant_half = [&](const Raw& R, int s, Ops& D, int v) {
+    const int u = v >> 1;
+    if (v & 1) {
+      if (u < TM) dequant4<1>(R.a[u][s], sp[u], D.a[u]);
+      else dequant4<1>(R.w[u - TM][s], sp[u], D.w[u - TM]);
+    } else if (u < TM) {
+      sp[u] = scale_pair(R.sa[u], s >> 1);
+      dequant4<0>(R.a[u][s], sp[u], D.a[u]);
+    } else {
+      sp[u] = scale_pair(R.sw[u - TM], s >> 1);
+      dequant4<0>(R.w[u - TM][s], sp[u], D.w[u - TM]);
+    }
+  };
   // W as the first operand: the accumulator block is the transposed output tile
   auto mfma_one = [&](const Ops& D, int q) {
     const int i = q / TN, j = q % TN;
@@ -284,8 +311,10 @@ __device__ __forceinline__ void gemm_tile(
     Ops D0, D1;
     // One K step, its raw operands in Rc and sub-step 0 already dequantized
     // in D0.  Sub-step s runs its MFMAs on D[s % 2] while the next sub-step
-    // is dequantized into the other buffer (one tile after every
-    // kMfmas / kTiles MFMAs).  After the first two MFMAs: the wait for
+    // is dequantized into the other buffer, half a tile (four conversions
+    // and four multiplies) after each MFMA or so, evenly spread: a lone
+    // wavefront per SIMD issues its MFMAs on time only when no MFMA is
+    // followed by a whole tile's conversions.  After the first two MFMAs: the wait for
     // stage kt+1 and the barrier (stage kt+1 landed everywhere, everyone done
     // reading stage kt's slot, which is refilled with stage kt+S).  During
     // sub-step 1 the raw tiles of stage kt+1 are read into Rn; sub-step 3
@@ -319,10 +348,10 @@ __device__ __forceinline__ void gemm_tile(
             __builtin_amdgcn_sched_barrier(0);
           }
 #pragma unroll
-          for (int u = 0; u < kTiles; ++u)
-            if ((u * kMfmas) / kTiles == q) {
-              if (s < 3) dequant_one(Rc, s + 1, Dn, u);
-              else dequant_one(Rn, 0, Dn, u);
+          for (int v = 0; v < 2 * kTiles; ++v)
+            if ((v * kMfmas) / (2 * kTiles) == q) {
+              if (s < 3) dequant_half(Rc, s + 1, Dn, v);
+              else dequant_half(Rn, 0, Dn, v);
             }
         }
       }
