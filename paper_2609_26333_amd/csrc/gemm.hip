@@ -614,7 +614,7 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
   // bf16 output without SwiGLU on grids of at least two full rounds of
   // 256x256 tiles: one workgroup of four 128x128 wavefronts per compute unit
   // (one wavefront per SIMD, 256 accumulator registers).  A wavefront
-  // dequantizes a quarter fewer operand elements per MFMA than a 128x64 one;
+  // dequantizes a third fewer operand elements per MFMA than a 128x64 one;
   // on such grids that outweighs the lost overlap between two workgroups
   // (27B down-projection at M = 32768 4-5 % faster, M = 8192 3 %, the 8B
   // down-projection at M = 8192 6 %, the 27B gate/up shape at M = 4096 2 %).
