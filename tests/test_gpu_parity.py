@@ -267,15 +267,16 @@ def test_gemm_tile_geometries_agree(M, N, K, out):
         PB.assert_within(y, ref, bound, "geometries bf16", bf16=True)
 
 
-@pytest.mark.parametrize("M,N,K", [(4096, 8192, 128), (4000, 8320, 192), (4096, 16640, 64)])
+@pytest.mark.parametrize("M,N,K", [(4096, 8192, 128), (4000, 8320, 192), (4096, 16640, 64), (4096, 8192, 80)])
 def test_gemm_wide_tile_geometry_agrees(M, N, K):
     """bf16 outputs of grids of at least two rounds of 256x256 tiles run as
     one workgroup of four 128x128 wavefronts per compute unit (with a partial
     last round of 256x128 tiles in the trailing columns when N is not a whole
     number of rounds); 32-row slices launch the small-tile geometry.  Every
     output is accumulated over K in the same order, so the slices equal the
-    full call bit for bit (ragged rows and edge columns included), and
-    sampled rows of the full call match the oracle."""
+    full call bit for bit (ragged rows, edge columns and a K that ends inside
+    a 64-column step included), and sampled rows of the full call match the
+    oracle."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     assert ((M + 255) // 256) * ((N + 255) // 256) >= 2 * cus, "shape must take the 256x256 geometry"
     say("wide geometry", M, N, K)
