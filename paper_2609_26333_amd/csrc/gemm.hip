@@ -228,6 +228,22 @@ __device__ __forceinline__ void gemm_tile(
   }
   const int s_m0 = Gm::a_scales + wave * SPW * 256;
   // stage kt into ring slot `slot` (kt past the end: the last one again)
+  // load r (0 .. CPW + SPW - 1) of stage kt into ring slot `slot`
+  auto issue_one = [&](int kt, int slot, auto rc) {
+    constexpr int r = decltype(rc)::value;
+    uint8_t* stage = smem + slot * Gm::bytes;
+    const int ktc = kt < KTi ? kt : KTi - 1;
+    if constexpr (r < CPW) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(c_a[r] ? rac : rwc,
+                                               (__attribute__((address_space(3))) void*)(stage + c_m0), 16,
+                                               c_off[r], ktc * 1024, r * 1024, 0);
+    } else {
+      constexpr int u = r - CPW;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(s_a[u] ? ras : rws,
+                                               (__attribute__((address_space(3))) void*)(stage + s_m0), 4,
+                                               s_off[u], ktc * 128, u * 256, 0);
+    }
+  };
   auto issue = [&](int kt, int slot) {
     uint8_t* stage = smem + slot * Gm::bytes;
     const int ktc = kt < KTi ? kt : KTi - 1;
@@ -316,7 +332,8 @@ __device__ __forceinline__ void gemm_tile(
     // wavefront per SIMD issues its MFMAs on time only when no MFMA is
     // followed by a whole tile's conversions.  After the first two MFMAs: the wait for
     // stage kt+1 and the barrier (stage kt+1 landed everywhere, everyone done
-    // reading stage kt's slot, which is refilled with stage kt+S).  During
+    // reading stage kt's slot, which is refilled with stage kt+S, one load
+    // per MFMA from the third on).  During
     // sub-step 1 the raw tiles of stage kt+1 are read into Rn; sub-step 3
     // dequantizes sub-step 0 of the next step from them.  The sched_barrier
     // fences keep this order; the empty asm statements pin the accumulators
@@ -338,7 +355,15 @@ __device__ __forceinline__ void gemm_tile(
           if (s == 0 && q == 1) {
             wait_vm<(S - 2) * L>();
             lds_barrier();
-            issue(kt + S, slot);
+            if (2 + L > kMfmas) issue(kt + S, slot);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          // the refill of stage kt's slot, one load after each of the next
+          // MFMAs (all at once when the sub-step has too few of them)
+          if (2 + L <= kMfmas && s == 0 && q >= 2 && q < 2 + L) {
+            static_for<0, L>([&](auto rc) {
+              if (q == 2 + decltype(rc)::value) issue_one(kt + S, slot, rc);
+            });
             __builtin_amdgcn_sched_barrier(0);
           }
           if (s == 1) {
