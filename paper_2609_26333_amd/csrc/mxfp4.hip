@@ -249,6 +249,21 @@ __device__ __forceinline__ void mx_gemm_tile(int64_t blk, const MxPanels& P, con
   const uint32_t s_off = (uint32_t)(sg * KT * 256 + lane * 4 + kBias);
   const int s_dst = Gm::a_scales + si * 256;
   // stage kt into the ring slot at byte offset `off` (kt past the end: the last one again)
+  // load r (0 .. L-1) of stage kt into the ring slot at byte offset `off`
+  auto issue_one = [&](int kt, int off, auto rc) {
+    constexpr int r = decltype(rc)::value;
+    uint8_t* stage = smem + off;
+    const int ktc = kt < KTi ? kt : KTi - 1;
+    if constexpr (r < CPW) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(c_a[r] ? rac : rwc,
+                                               (__attribute__((address_space(3))) void*)(stage + c_m0), 16,
+                                               c_off[r], ktc * 1024, r * 1024, 0);
+    } else {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(s_is_a ? ras : rws,
+                                               (__attribute__((address_space(3))) void*)(stage + s_dst), 4, s_off,
+                                               ktc * 256, 0, 0);
+    }
+  };
   auto issue = [&](int kt, int off) {
     uint8_t* stage = smem + off;
     const int ktc = kt < KTi ? kt : KTi - 1;
@@ -314,6 +329,7 @@ __device__ __forceinline__ void mx_gemm_tile(int64_t blk, const MxPanels& P, con
   };
   constexpr int kMfmas = TM * TN;
   constexpr int kSlots = kMfmas > kReads + 3 ? kMfmas : kReads + 3;
+  static_assert(3 + L <= kSlots, "every refill load has a slot in the step");
 
   if (KTi > 0) {
     // prologue: stages 0 .. S-1 in flight, stage 0 landed everywhere
@@ -325,8 +341,10 @@ __device__ __forceinline__ void mx_gemm_tile(int64_t blk, const MxPanels& P, con
     // One step (cur = stage kt's operands, read during the previous step):
     // two MFMAs are issued before the wait for stage kt+1 and the barrier so
     // that the matrix cores stay busy through them; after the barrier the
-    // slot of stage kt (read by everyone) is refilled with stage kt+S and the
-    // reads of stage kt+1 are interleaved with the remaining MFMAs.  The
+    // slot of stage kt (read by everyone) is refilled with stage kt+S, one
+    // load after each MFMA (issued in a burst they held back the MFMAs that
+    // followed), and the reads of stage kt+1 are interleaved with the
+    // remaining MFMAs.  The
     // sched_barriers keep this order; the empty asm statements pin the
     // accumulators at the end of the step (otherwise the compiler sinks the
     // MFMAs, pure register operations, into the next step).
@@ -341,11 +359,13 @@ __device__ __forceinline__ void mx_gemm_tile(int64_t blk, const MxPanels& P, con
       mx_barrier();
       mfma_one(cur, 2);
       __builtin_amdgcn_sched_barrier(0);
-      issue(kt + S, off);
       const uint8_t* stg = smem + noff;
 #pragma unroll
       for (int q = 3; q < kSlots; ++q) {
         __builtin_amdgcn_sched_barrier(0);
+        static_for<0, L>([&](auto rc) {
+          if (q == 3 + decltype(rc)::value) issue_one(kt + S, off, rc);
+        });
         if (q - 3 < kReads) read_one(stg, nxt, q - 3);
         __builtin_amdgcn_sched_barrier(0);
         if (q < kMfmas) mfma_one(cur, q);
