@@ -59,37 +59,37 @@ __device__ inline int floor_log2(float a) {
 
 // ---------------------------------------------------------------- quantizer
 // One workgroup per 4-tile scale group: wavefront q quantizes the 32x64 tile
-// (4g + q, tc); lane l = row l%32, columns 32*(l/32)..+31 of the tile (one
-// MX block).  Codes: the lane's 16 bytes at 32*(l%32) + 16*(l/32) of the tile
-// (row-major 32 bytes per row).  Scales: byte 4l + q of the group's 256, so
-// that one dword per lane carries the scales of 4 row tiles (the GEMM's
-// operand).  Rows past `rows` and columns past `cols` produce zero codes and
-// scale code 0; tiles past the last row tile (group padding) get scale 0 only.
+// (4g + q, tc) in four passes of eight rows, eight lanes per row (8 elements
+// each, so that a load instruction reads 128 contiguous bytes of each of 8
+// bf16 rows); an MX block is the 4 lanes of a row that share its 32 columns,
+// which exchange their maxima.  Codes: row-major 32 bytes per row of the
+// tile, a lane's 4 bytes at 32 r + 4 (l % 8).  Scales: byte 4(r + 32h) + q of
+// the group's 256 for row r and column half h, so that one dword per lane
+// carries the scales of 4 row tiles (the GEMM's operand).  Rows past `rows`
+// and columns past `cols` produce zero codes and scale code 0; tiles past the
+// last row tile (group padding) get scale 0 only.
+// Eight consecutive elements as fp32 (one 16-byte load for bf16, two for fp32).
 template <typename T>
-__device__ inline void load_block(const T* __restrict__ src, float (&v)[32]);
+__device__ inline void load8(const T* __restrict__ src, float (&v)[8]);
 
 template <>
-__device__ inline void load_block<uint16_t>(const uint16_t* __restrict__ src, float (&v)[32]) {
+__device__ inline void load8<uint16_t>(const uint16_t* __restrict__ src, float (&v)[8]) {
+  const uint4_t w = *reinterpret_cast<const uint4_t*>(src);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const uint4_t w = *reinterpret_cast<const uint4_t*>(src + 8 * q);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v[8 * q + 2 * i] = bf16_lo(w[i]);
-      v[8 * q + 2 * i + 1] = bf16_hi(w[i]);
-    }
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = bf16_lo(w[i]);
+    v[2 * i + 1] = bf16_hi(w[i]);
   }
 }
 
 template <>
-__device__ inline void load_block<float>(const float* __restrict__ src, float (&v)[32]) {
+__device__ inline void load8<float>(const float* __restrict__ src, float (&v)[8]) {
+  const float4_t w0 = *reinterpret_cast<const float4_t*>(src);
+  const float4_t w1 = *reinterpret_cast<const float4_t*>(src + 4);
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const float4_t w = *reinterpret_cast<const float4_t*>(src + 4 * q);
-    v[4 * q] = w[0];
-    v[4 * q + 1] = w[1];
-    v[4 * q + 2] = w[2];
-    v[4 * q + 3] = w[3];
+  for (int i = 0; i < 4; ++i) {
+    v[i] = w0[i];
+    v[4 + i] = w1[i];
   }
 }
 
@@ -101,37 +101,45 @@ __global__ __launch_bounds__(256) void mx_quantize_kernel(const T* __restrict__ 
   const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
   const int64_t g = blockIdx.x / tiles_c, tc = blockIdx.x - g * tiles_c;
   const int64_t tr = 4 * g + q;
-  const int r = lane & 31, h = lane >> 5;
-  const int64_t row = tr * 32 + r, col = tc * 64 + h * 32;
-  float v[32];
-  if (row < rows && col < cols) {
-    load_block<T>(x + row * cols + col, v);
-  } else {
+  // eight lanes per row (8 elements each: 128 contiguous bytes of bf16 per
+  // row and load), eight rows per pass, four passes; an MX block is the
+  // 4 lanes c & ~3 .. c | 3 of a row
+  const int c = lane & 7, rr = lane >> 3;
+  const int64_t col = tc * 64 + c * 8;
+  const int64_t cc = min(col, cols - 8);   // cols % 32 == 0
+  float v[4][8];
+  bool ok[4];
 #pragma unroll
-    for (int i = 0; i < 32; ++i) v[i] = 0.0f;
+  for (int i = 0; i < 4; ++i) {
+    const int64_t row = tr * 32 + 8 * i + rr;
+    ok[i] = row < rows && col < cols;
+    load8<T>(x + min(row, rows - 1) * cols + cc, v[i]);
   }
-  float a = 0.0f;
+  uint8_t* sg = reinterpret_cast<uint8_t*>(s_grp);
 #pragma unroll
-  for (int i = 0; i < 32; ++i) a = fmaxf(a, fabsf(v[i]));
-  int e = a > 0.0f ? floor_log2(a) - 2 : -127;
-  e = e < -127 ? -127 : (e > 127 ? 127 : e);
-  // 2^-e as fp32: -e lies in [-125, 127] for finite inputs (a < 2^128 gives
-  // e <= 125), so the biased exponent 127 - e is in [2, 254]
-  const float p = __uint_as_float((uint32_t)(127 - e) << 23);
-  if (tr < tiles_r) {
-    uint4_t out;
+  for (int i = 0; i < 4; ++i) {
+    float a = 0.0f;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      uint32_t w = 0u;
-      w = cvt_pk_fp4<0>(w, v[8 * k] * p, v[8 * k + 1] * p);
-      w = cvt_pk_fp4<1>(w, v[8 * k + 2] * p, v[8 * k + 3] * p);
-      w = cvt_pk_fp4<2>(w, v[8 * k + 4] * p, v[8 * k + 5] * p);
-      w = cvt_pk_fp4<3>(w, v[8 * k + 6] * p, v[8 * k + 7] * p);
-      out[k] = fp4_canonical_zero(w);
+    for (int k = 0; k < 8; ++k) {
+      v[i][k] = ok[i] ? v[i][k] : 0.0f;
+      a = fmaxf(a, fabsf(v[i][k]));
     }
-    *reinterpret_cast<uint4_t*>(codes + (tr * tiles_c + tc) * 1024 + r * 32 + h * 16) = out;
+    a = fmaxf(a, __shfl_xor(a, 1, 64));
+    a = fmaxf(a, __shfl_xor(a, 2, 64));
+    int e = a > 0.0f ? floor_log2(a) - 2 : -127;
+    e = e < -127 ? -127 : (e > 127 ? 127 : e);
+    const float p = __uint_as_float((uint32_t)(127 - e) << 23);
+    const int r = 8 * i + rr;
+    if (tr < tiles_r) {
+      uint32_t w = 0u;
+      w = cvt_pk_fp4<0>(w, v[i][0] * p, v[i][1] * p);
+      w = cvt_pk_fp4<1>(w, v[i][2] * p, v[i][3] * p);
+      w = cvt_pk_fp4<2>(w, v[i][4] * p, v[i][5] * p);
+      w = cvt_pk_fp4<3>(w, v[i][6] * p, v[i][7] * p);
+      *reinterpret_cast<uint32_t*>(codes + (tr * tiles_c + tc) * 1024 + r * 32 + c * 4) = fp4_canonical_zero(w);
+    }
+    if ((c & 3) == 0) sg[4 * (r + 32 * (c >> 2)) + q] = (uint8_t)(e + 127);
   }
-  reinterpret_cast<uint8_t*>(s_grp)[4 * lane + q] = (uint8_t)(e + 127);
   __syncthreads();
   if (q == 0) reinterpret_cast<uint32_t*>(scales + (g * tiles_c + tc) * 256)[lane] = s_grp[lane];
 }
